@@ -1,0 +1,166 @@
+/*
+ * upr.h - C interface of the candidate-ranking library (MI355X / gfx950).
+ *
+ * The library implements the ranking half of UniPinRec's cross-stage KV-cache
+ * sharing (paper Sec. 3, "Overall serving design" and "KV-cache sharing
+ * across stages"): a shared transformer encodes each user's action history
+ * once and keeps every layer's keys and values; ranking then runs only the
+ * candidate tokens through the same transformer, each candidate attending to
+ * its user's cached history keys plus its own key and never to another
+ * candidate (Sec. 3, "Masked Action Modeling", attention-pattern item), and
+ * returns one score per candidate.
+ *
+ * Conventions shared by every call:
+ *   - All functions are extern "C"; no C++ exception crosses this boundary.
+ *   - "host" pointers are ordinary CPU memory, "device" pointers are HIP
+ *     device memory on the current device.  The caller owns every buffer it
+ *     passes; the library never frees or retains them beyond the call (the
+ *     kernels it enqueues read/write them until they finish on `stream`).
+ *   - `stream` is a hipStream_t passed as void*; NULL means the null stream.
+ *     encode/rank enqueue work and return without synchronising.  A fault in
+ *     a kernel surfaces at the caller's next synchronisation.
+ *   - Arguments are validated on the host before anything is enqueued.  On a
+ *     non-UPR_OK return nothing has been enqueued and no output byte has been
+ *     written; upr_last_error() then gives a description (thread-local).
+ *   - Row segments: offsets are int32, num_users+1 entries, non-decreasing,
+ *     offsets[0] >= 0.  User u owns packed rows offsets[u] .. offsets[u+1]-1.
+ *     offsets[0] > 0 is allowed (a call on a sub-range of a shared buffer).
+ *     Empty users (equal consecutive offsets) are allowed.
+ *   - A model is immutable after creation and may be used from several host
+ *     threads at once; concurrent calls need distinct workspaces and must
+ *     not write the same outputs.
+ */
+#ifndef UPR_H
+#define UPR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    UPR_OK = 0,
+    UPR_ERR_NULL = 1,       /* a required pointer is NULL                      */
+    UPR_ERR_CONFIG = 2,     /* unsupported model shape                         */
+    UPR_ERR_OFFSETS = 3,    /* malformed or mismatched segment offsets         */
+    UPR_ERR_CAPACITY = 4,   /* history rows exceed the cache capacity          */
+    UPR_ERR_WORKSPACE = 5,  /* workspace too small or misaligned               */
+    UPR_ERR_DTYPE = 6,      /* unknown arithmetic type                         */
+    UPR_ERR_HIP = 7,        /* a HIP runtime call failed                       */
+    UPR_ERR_WEIGHTS = 8     /* weight blob has the wrong number of values      */
+} upr_status;
+
+typedef enum { UPR_F32 = 0, UPR_BF16 = 1 } upr_dtype;
+
+/* Model shape.  Supported: head_dim in {32, 64}; d_model = n_heads*head_dim,
+ * a multiple of 64 and at most 1024; d_ff a multiple of 64 and at most 8192;
+ * 1 <= n_layers <= 64.  dtype selects the storage/arithmetic type of
+ * activations, weights, tokens and cache: UPR_F32 computes in fp32
+ * throughout; UPR_BF16 stores bf16 and accumulates every contraction,
+ * normalisation and softmax in fp32.  ln_eps is the LayerNorm epsilon. */
+typedef struct {
+    int32_t d_model;
+    int32_t n_heads;
+    int32_t head_dim;
+    int32_t n_layers;
+    int32_t d_ff;
+    int32_t dtype;          /* a upr_dtype value */
+    float ln_eps;
+} upr_config;
+
+typedef struct upr_model upr_model;     /* opaque */
+
+/* Packed row segments of one call (see the conventions above). */
+typedef struct {
+    int32_t num_users;
+    const int32_t* offsets_host;    /* host, num_users+1 entries              */
+    const int32_t* offsets_dev;     /* device, the same num_users+1 values    */
+} upr_segments;
+
+/* Packed per-layer K/V cache (device memory, caller-owned).
+ * Layout [n_layers][2][n_heads][capacity_rows][head_dim] of the model's dtype:
+ * per layer a K plane then a V plane, heads outermost inside a plane, then
+ * one row per packed history token (history row r of the encode call is cache
+ * row r), then the head's features.  Element (l, kv, h, r, e) sits at
+ * upr_kv_cache_index(...).  Each (layer, kv, head, user) block is one
+ * contiguous slab of n_u*head_dim elements. */
+typedef struct {
+    void* data;
+    int64_t capacity_rows;
+} upr_kv_cache;
+
+/* Number of float values in the weight blob for `cfg`, or -1 if cfg is invalid.
+ * Blob order (all float32, linear weights [out, in]), per layer l:
+ *   ln1_g[d] ln1_b[d] Wq[d,d] bq[d] Wk[d,d] bk[d] Wv[d,d] bv[d] Wo[d,d] bo[d]
+ *   ln2_g[d] ln2_b[d] W1[F,d] b1[F] W2[d,F] b2[d]
+ * then lnf_g[d] lnf_b[d] w_score[d] b_score[1]. */
+int64_t upr_weights_count(const upr_config* cfg);
+
+/* Create a model: copies the host blob (weights_count floats) to device
+ * memory.  For UPR_BF16 the matrices are rounded to bf16 (nearest, ties to
+ * even) and the vectors (gains, shifts, biases, score weights) kept in fp32.
+ * This is the only call that allocates device memory.  The blob may be freed
+ * after return.  *out is set only on UPR_OK. */
+upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
+                            int64_t weights_count, upr_model** out);
+
+/* Release a model (NULL is ignored).  No call may be using it. */
+void upr_model_destroy(upr_model* model);
+
+/* Bytes of a cache with `capacity_rows` rows for cfg (0 if cfg is invalid). */
+size_t upr_kv_cache_bytes(const upr_config* cfg, int64_t capacity_rows);
+
+/* Element index of (layer, kv [0 = K, 1 = V], head, row, e) in the cache,
+ * computed in int64; -1 if any coordinate is out of range. */
+int64_t upr_kv_cache_index(const upr_config* cfg, int64_t capacity_rows, int32_t layer,
+                           int32_t kv, int32_t head, int64_t row, int32_t e);
+
+/* Workspace bytes needed by upr_encode_user for `hist` (0 on invalid input). */
+size_t upr_encode_workspace_bytes(const upr_model* model, const upr_segments* hist);
+
+/* Workspace bytes needed by upr_rank_candidates (0 on invalid input). */
+size_t upr_rank_workspace_bytes(const upr_model* model, const upr_segments* hist,
+                                const upr_segments* cand);
+
+/* History encoding (paper Sec. 3, "KV-cache sharing across stages": the
+ * O(n^2) history pass whose keys and values ranking reuses).
+ * hist_emb: device, [rows, d_model] of the model dtype, row-major, holding the
+ * packed history tokens (rows hist->offsets_host[0] .. [num_users]-1 are read).
+ * For each user and layer l, the causal transformer (position t attends to
+ * positions 0..t of the same user) writes that layer's keys and values of the
+ * user's rows into cache plane l.  Only those cache rows are written.
+ * ws: device workspace of at least upr_encode_workspace_bytes, 256-byte
+ * aligned; its contents are scratch. */
+upr_status upr_encode_user(const upr_model* model, const void* hist_emb,
+                           const upr_segments* hist, const upr_kv_cache* cache,
+                           void* ws, size_t ws_bytes, void* stream);
+
+/* Candidate ranking (paper Sec. 3, "Overall serving design": an incremental
+ * forward pass in which only candidate tokens are processed, attending back to
+ * the cached history).
+ * cand_emb: device, [rows, d_model] of the model dtype; rows
+ * cand->offsets_host[0] .. [num_users]-1 are read.  Candidate c of user u
+ * attends, at every layer, to the cached keys/values of rows
+ * hist->offsets[u] .. hist->offsets[u+1]-1 plus its own key/value, and to no
+ * other candidate.  scores: device float32, indexed like cand_emb rows; each
+ * row in range receives w . LayerNorm_f(h_c) + b (a raw logit).  The cache is
+ * only read, so several rank calls may share one cache.  hist and cand must
+ * have the same num_users.  ws: as for encode. */
+upr_status upr_rank_candidates(const upr_model* model, const upr_kv_cache* cache,
+                               const upr_segments* hist, const void* cand_emb,
+                               const upr_segments* cand, float* scores,
+                               void* ws, size_t ws_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* upr_status_string(int32_t status);
+
+/* Description of the last failure on the calling thread ("" if none). */
+const char* upr_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UPR_H */

@@ -1,0 +1,537 @@
+// Host side of the C interface: argument validation, model creation,
+// workspace carving and the encode / rank launch sequences.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <type_traits>
+#include <vector>
+
+#include "upr_internal.h"
+#include "upr_plan.h"
+
+using upr::bf16;
+
+struct upr_model {
+    upr_config cfg;
+    void* dev = nullptr;
+    size_t dev_bytes = 0;
+    upr::LayerWeights layers[upr::kMaxLayers];
+    upr::FinalWeights fin;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+upr_status fail(upr_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+upr_status ok() {
+    g_last_error.clear();
+    return UPR_OK;
+}
+
+upr_status check_config(const upr_config* c) {
+    if (!c) return fail(UPR_ERR_NULL, "config is NULL");
+    if (c->dtype != UPR_F32 && c->dtype != UPR_BF16)
+        return fail(UPR_ERR_DTYPE, "dtype %d is neither UPR_F32 nor UPR_BF16", c->dtype);
+    if (c->head_dim != 32 && c->head_dim != 64)
+        return fail(UPR_ERR_CONFIG, "head_dim %d not supported (32 or 64)", c->head_dim);
+    if (c->n_heads <= 0 || (int64_t)c->n_heads * c->head_dim != c->d_model)
+        return fail(UPR_ERR_CONFIG, "d_model %d != n_heads %d * head_dim %d", c->d_model,
+                    c->n_heads, c->head_dim);
+    if (c->d_model % 64 != 0 || c->d_model > 1024)
+        return fail(UPR_ERR_CONFIG, "d_model %d must be a multiple of 64 and <= 1024", c->d_model);
+    if (c->d_ff <= 0 || c->d_ff % 64 != 0 || c->d_ff > 8192)
+        return fail(UPR_ERR_CONFIG, "d_ff %d must be a positive multiple of 64, <= 8192", c->d_ff);
+    if (c->n_layers < 1 || c->n_layers > upr::kMaxLayers)
+        return fail(UPR_ERR_CONFIG, "n_layers %d outside [1, %d]", c->n_layers, upr::kMaxLayers);
+    if (!(c->ln_eps > 0.f) || !std::isfinite(c->ln_eps))
+        return fail(UPR_ERR_CONFIG, "ln_eps must be positive and finite");
+    return UPR_OK;
+}
+
+int64_t weights_count(const upr_config& c) {
+    const int64_t d = c.d_model, F = c.d_ff;
+    return c.n_layers * (4 * d * d + 2 * F * d + 9 * d + F) + 3 * d + 1;
+}
+
+uint16_t f32_to_bf16_rne(float f) {
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu))
+        return (uint16_t)((u >> 16) | 0x0040u);           // quiet NaN
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+float bf16_value(uint16_t b) {
+    const uint32_t u = (uint32_t)b << 16;
+    float f;
+    std::memcpy(&f, &u, 4);
+    return f;
+}
+
+// Validates one segment descriptor; on success [*first, *last) is its row range.
+upr_status check_segments(const upr_segments* s, const char* name, int64_t* first, int64_t* last) {
+    if (!s) return fail(UPR_ERR_NULL, "%s segments pointer is NULL", name);
+    if (s->num_users < 0) return fail(UPR_ERR_OFFSETS, "%s num_users %d < 0", name, s->num_users);
+    if (!s->offsets_host) return fail(UPR_ERR_NULL, "%s offsets_host is NULL", name);
+    const int32_t* o = s->offsets_host;
+    if (o[0] < 0) return fail(UPR_ERR_OFFSETS, "%s offsets[0] = %d < 0", name, o[0]);
+    for (int u = 0; u < s->num_users; ++u)
+        if (o[u + 1] < o[u])
+            return fail(UPR_ERR_OFFSETS, "%s offsets decrease at user %d (%d -> %d)", name, u, o[u],
+                        o[u + 1]);
+    if (s->num_users > 0 && !s->offsets_dev)
+        return fail(UPR_ERR_NULL, "%s offsets_dev is NULL", name);
+    *first = o[0];
+    *last = o[s->num_users];
+    return UPR_OK;
+}
+
+upr_status check_workspace(void* ws, size_t ws_bytes, size_t need) {
+    if (need == 0) return UPR_OK;
+    if (!ws) return fail(UPR_ERR_NULL, "workspace is NULL (%zu bytes needed)", need);
+    if (ws_bytes < need)
+        return fail(UPR_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, need);
+    if (reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+        return fail(UPR_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+    return UPR_OK;
+}
+
+#define UPR_HIP(...)                                                                            \
+    do {                                                                                        \
+        hipError_t e_ = (__VA_ARGS__);                                                          \
+        if (e_ != hipSuccess)                                                                   \
+            return fail(UPR_ERR_HIP, "%s failed: %s", #__VA_ARGS__, hipGetErrorString(e_));     \
+    } while (0)
+
+size_t elem_size(const upr_config& c) { return c.dtype == UPR_BF16 ? 2 : 4; }
+
+void* plane_ptr(const upr_config& c, const upr_kv_cache* cache, int layer, int kv) {
+    const size_t off = (size_t)(layer * 2 + kv) * c.n_heads * cache->capacity_rows * c.head_dim;
+    return static_cast<char*>(cache->data) + off * elem_size(c);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Encode / rank sequences
+// ---------------------------------------------------------------------------
+namespace upr {
+
+// Attention-output projection and FFN of one layer, on the fp32 residual g:
+// g += o Wo^T + bo;  a = LN2(g);  h = gelu(a W1^T + b1);  g += h W2^T + b2.
+template <typename Types>
+static hipError_t launch_ffn_block(const LayerWeights& w, const typename Types::act* o,
+                                   typename Types::act* a, typename Types::act* h, float* g,
+                                   int64_t R, int d, int F, float eps, hipStream_t s) {
+    using T = typename Types::kv;
+    using TA = typename Types::act;
+    Epilogue r{};
+    r.mode = EPI_RESID;
+    r.acc_scale = w.s_o;
+    r.bias = w.bo;
+    r.resid = g;
+    r.ldr = d;
+    hipError_t e = launch_gemm<TA, T>(o, d, static_cast<const TA*>(w.Wo), R, d, d, r, s);
+    if (e != hipSuccess) return e;
+    e = launch_layernorm<TA>(g, a, R, d, w.ln2_g, w.ln2_b, eps, s);
+    if (e != hipSuccess) return e;
+    Epilogue up{};
+    up.mode = EPI_GELU;
+    up.acc_scale = w.s_1;
+    up.bias = w.b1;
+    up.out = h;
+    up.ldo = F;
+    e = launch_gemm<TA, T>(a, d, static_cast<const TA*>(w.W1), R, F, d, up, s);
+    if (e != hipSuccess) return e;
+    r.acc_scale = w.s_2;
+    r.bias = w.b2;
+    return launch_gemm<TA, T>(h, F, static_cast<const TA*>(w.W2), R, d, F, r, s);
+}
+
+template <typename Types>
+static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_emb,
+                             const upr_segments* hist, const upr_kv_cache* cache,
+                             const EncodePlan& p, char* ws, hipStream_t s) {
+    using T = typename Types::kv;
+    using TA = typename Types::act;
+    const upr_config& c = m->cfg;
+    const int d = c.d_model, F = c.d_ff, H = c.n_heads, D = c.head_dim;
+    const int64_t R = p.rows;
+    float* g = reinterpret_cast<float*>(ws + p.off_g);
+    TA* a = reinterpret_cast<TA*>(ws + p.off_a);
+    T* q = reinterpret_cast<T*>(ws + p.off_q);
+    TA* o = reinterpret_cast<TA*>(ws + p.off_o);
+    TA* h = reinterpret_cast<TA*>(ws + p.off_h);
+    const float qscale = 1.4426950408889634f / std::sqrt((float)D);
+    UPR_HIP(launch_resid_init<T>(hist_emb + p.row0 * d, g, R, d, s));
+    for (int l = 0; l < c.n_layers; ++l) {
+        const LayerWeights& w = m->layers[l];
+        UPR_HIP(launch_layernorm<TA>(g, a, R, d, w.ln1_g, w.ln1_b, c.ln_eps, s));
+        Epilogue e{};
+        e.mode = EPI_QKV_CACHE;
+        e.acc_scale = w.s_qkv;
+        e.bias = w.bqkv;
+        e.out = q;
+        e.ldo = d;
+        e.col_scale = qscale;
+        e.scale_cols = d;
+        e.cache_k = plane_ptr(c, cache, l, 0);
+        e.cache_v = plane_ptr(c, cache, l, 1);
+        e.cache_cap = cache->capacity_rows;
+        e.row0 = p.row0;
+        e.d_model = d;
+        e.head_dim = D;
+        UPR_HIP(launch_gemm<TA, T>(a, d, static_cast<const TA*>(w.Wqkv), R, 3 * d, d, e, s));
+        if (l == c.n_layers - 1) break;     // the cache is complete; nothing reads further
+        UPR_HIP(launch_attn_encode_simple<T, TA>(q, o, R, p.row0, H, D, hist->offsets_dev,
+                                             hist->num_users,
+                                             static_cast<const T*>(e.cache_k),
+                                             static_cast<const T*>(e.cache_v),
+                                             cache->capacity_rows, s));
+        UPR_HIP(launch_ffn_block<Types>(w, o, a, h, g, R, d, F, c.ln_eps, s));
+    }
+    return UPR_OK;
+}
+
+template <typename Types>
+static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
+                           const upr_segments* hist, const typename Types::kv* cand_emb,
+                           const upr_segments* cand, float* scores, const RankPlan& p, char* ws,
+                           hipStream_t s) {
+    using T = typename Types::kv;
+    using TA = typename Types::act;
+    const upr_config& c = m->cfg;
+    const int d = c.d_model, F = c.d_ff, H = c.n_heads, D = c.head_dim;
+    const int64_t R = p.rows;
+    float* g = reinterpret_cast<float*>(ws + p.off_g);
+    TA* a = reinterpret_cast<TA*>(ws + p.off_a);
+    T* qkv = reinterpret_cast<T*>(ws + p.off_qkv);
+    TA* o = reinterpret_cast<TA*>(ws + p.off_o);
+    TA* h = reinterpret_cast<TA*>(ws + p.off_h);
+    const float qscale = 1.4426950408889634f / std::sqrt((float)D);
+    UPR_HIP(launch_resid_init<T>(cand_emb + p.row0 * d, g, R, d, s));
+    if (p.use_mfma_attn)
+        UPR_HIP(launch_rank_worklist(cand->offsets_dev, hist->offsets_dev, cand->num_users, H,
+                                     p.attn_tile, reinterpret_cast<int32_t*>(ws + p.off_work),
+                                     p.work_items, s));
+    for (int l = 0; l < c.n_layers; ++l) {
+        const LayerWeights& w = m->layers[l];
+        UPR_HIP(launch_layernorm<TA>(g, a, R, d, w.ln1_g, w.ln1_b, c.ln_eps, s));
+        Epilogue e{};
+        e.mode = EPI_STORE;
+        e.acc_scale = w.s_qkv;
+        e.bias = w.bqkv;
+        e.out = qkv;
+        e.ldo = 3 * d;
+        e.col_scale = qscale;
+        e.scale_cols = d;
+        UPR_HIP(launch_gemm<TA, T>(a, d, static_cast<const TA*>(w.Wqkv), R, 3 * d, d, e, s));
+        const T* ck = static_cast<const T*>(plane_ptr(c, cache, l, 0));
+        const T* cv = static_cast<const T*>(plane_ptr(c, cache, l, 1));
+        bool done = false;
+        if constexpr (std::is_same_v<Types, Bf16Types>) {
+            if (p.use_mfma_attn) {
+                UPR_HIP(launch_attn_rank(qkv, o, p.row0, H, D, cand->offsets_dev,
+                                         hist->offsets_dev,
+                                         reinterpret_cast<const int32_t*>(ws + p.off_work),
+                                         p.work_items, p.attn_tile, ck, cv, cache->capacity_rows,
+                                         s));
+                done = true;
+            }
+        }
+        if (!done)
+            UPR_HIP(launch_attn_rank_simple<T, TA>(qkv, o, R, p.row0, H, D, cand->offsets_dev,
+                                               hist->offsets_dev, cand->num_users, ck, cv,
+                                               cache->capacity_rows, s));
+        UPR_HIP(launch_ffn_block<Types>(w, o, a, h, g, R, d, F, c.ln_eps, s));
+    }
+    UPR_HIP(launch_score_head(g, scores + p.row0, R, d, m->fin, c.ln_eps, s));
+    return UPR_OK;
+}
+
+}  // namespace upr
+
+// ---------------------------------------------------------------------------
+// C interface
+// ---------------------------------------------------------------------------
+extern "C" {
+
+int64_t upr_weights_count(const upr_config* cfg) {
+    if (check_config(cfg) != UPR_OK) return -1;
+    return weights_count(*cfg);
+}
+
+upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
+                            int64_t count, upr_model** out) {
+    upr_status st = check_config(cfg);
+    if (st != UPR_OK) return st;
+    if (!weights_host) return fail(UPR_ERR_NULL, "weights_host is NULL");
+    if (!out) return fail(UPR_ERR_NULL, "out is NULL");
+    const upr_config c = *cfg;
+    if (count != weights_count(c))
+        return fail(UPR_ERR_WEIGHTS, "weight blob has %lld values, config needs %lld",
+                    (long long)count, (long long)weights_count(c));
+    const int64_t d = c.d_model, F = c.d_ff;
+    const size_t es = elem_size(c);
+    // Device image: per layer the four matrices (model dtype), then all
+    // vectors (fp32).  Every piece starts on a 256-byte boundary.
+    std::vector<char> img;
+    auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
+    // Matrices: fp32 models copy them; bf16 models round each value to bf16
+    // (nearest, ties to even), multiply by an exact power of two 2^k that puts
+    // the largest magnitude in [2^14, 2^15), and store fp16 -- exact for every
+    // value within 2^29 of that maximum.  *scale receives 2^-k.
+    auto add_mat = [&](const float* src, int64_t n, float* scale) {
+        size_t off = align(img.size());
+        img.resize(off + n * es);
+        *scale = 1.0f;
+        if (c.dtype == UPR_BF16) {
+            float maxabs = 0.f;
+            for (int64_t i = 0; i < n; ++i)
+                maxabs = std::fmax(maxabs, std::fabs(bf16_value(f32_to_bf16_rne(src[i]))));
+            int k = 0;
+            if (maxabs > 0.f && std::isfinite(maxabs)) {
+                int ex;
+                std::frexp(maxabs, &ex);               // maxabs in [2^(ex-1), 2^ex)
+                k = std::min(100, std::max(-100, 15 - ex));
+            }
+            const float up = std::ldexp(1.0f, k);
+            *scale = std::ldexp(1.0f, -k);
+            _Float16* dst = reinterpret_cast<_Float16*>(img.data() + off);
+            for (int64_t i = 0; i < n; ++i)
+                dst[i] = (_Float16)(bf16_value(f32_to_bf16_rne(src[i])) * up);
+        } else {
+            std::memcpy(img.data() + off, src, n * 4);
+        }
+        return off;
+    };
+    auto add_vec = [&](const float* src, int64_t n) {
+        size_t off = align(img.size());
+        img.resize(off + n * 4);
+        std::memcpy(img.data() + off, src, n * 4);
+        return off;
+    };
+    struct LayerOff {
+        size_t Wqkv, Wo, W1, W2, ln1_g, ln1_b, bqkv, bo, ln2_g, ln2_b, b1, b2;
+        float s_qkv, s_o, s_1, s_2;
+    };
+    std::vector<LayerOff> lo(c.n_layers);
+    const float* p = weights_host;
+    std::vector<float> tmp;
+    for (int l = 0; l < c.n_layers; ++l) {
+        const float* ln1_g = p; p += d;
+        const float* ln1_b = p; p += d;
+        const float* Wq = p; p += d * d;
+        const float* bq = p; p += d;
+        const float* Wk = p; p += d * d;
+        const float* bk = p; p += d;
+        const float* Wv = p; p += d * d;
+        const float* bv = p; p += d;
+        const float* Wo = p; p += d * d;
+        const float* bo = p; p += d;
+        const float* ln2_g = p; p += d;
+        const float* ln2_b = p; p += d;
+        const float* W1 = p; p += F * d;
+        const float* b1 = p; p += F;
+        const float* W2 = p; p += d * F;
+        const float* b2 = p; p += d;
+        tmp.assign(Wq, Wq + d * d);
+        tmp.insert(tmp.end(), Wk, Wk + d * d);
+        tmp.insert(tmp.end(), Wv, Wv + d * d);
+        lo[l].Wqkv = add_mat(tmp.data(), 3 * d * d, &lo[l].s_qkv);
+        lo[l].Wo = add_mat(Wo, d * d, &lo[l].s_o);
+        lo[l].W1 = add_mat(W1, F * d, &lo[l].s_1);
+        lo[l].W2 = add_mat(W2, d * F, &lo[l].s_2);
+        lo[l].ln1_g = add_vec(ln1_g, d);
+        lo[l].ln1_b = add_vec(ln1_b, d);
+        tmp.assign(bq, bq + d);
+        tmp.insert(tmp.end(), bk, bk + d);
+        tmp.insert(tmp.end(), bv, bv + d);
+        lo[l].bqkv = add_vec(tmp.data(), 3 * d);
+        lo[l].bo = add_vec(bo, d);
+        lo[l].ln2_g = add_vec(ln2_g, d);
+        lo[l].ln2_b = add_vec(ln2_b, d);
+        lo[l].b1 = add_vec(b1, F);
+        lo[l].b2 = add_vec(b2, d);
+    }
+    const size_t off_lnf_g = add_vec(p, d); p += d;
+    const size_t off_lnf_b = add_vec(p, d); p += d;
+    const size_t off_ws = add_vec(p, d); p += d;
+    const size_t off_bs = add_vec(p, 1); p += 1;
+    img.resize(align(img.size()));
+
+    upr_model* m = new upr_model();
+    m->cfg = c;
+    m->dev_bytes = img.size();
+    hipError_t e = hipMalloc(&m->dev, m->dev_bytes);
+    if (e != hipSuccess) {
+        delete m;
+        return fail(UPR_ERR_HIP, "hipMalloc(%zu) failed: %s", img.size(), hipGetErrorString(e));
+    }
+    e = hipMemcpy(m->dev, img.data(), img.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(m->dev);
+        delete m;
+        return fail(UPR_ERR_HIP, "hipMemcpy of weights failed: %s", hipGetErrorString(e));
+    }
+    char* base = static_cast<char*>(m->dev);
+    auto fp = [&](size_t off) { return reinterpret_cast<const float*>(base + off); };
+    for (int l = 0; l < c.n_layers; ++l) {
+        upr::LayerWeights& w = m->layers[l];
+        w.Wqkv = base + lo[l].Wqkv;
+        w.Wo = base + lo[l].Wo;
+        w.W1 = base + lo[l].W1;
+        w.W2 = base + lo[l].W2;
+        w.s_qkv = lo[l].s_qkv;
+        w.s_o = lo[l].s_o;
+        w.s_1 = lo[l].s_1;
+        w.s_2 = lo[l].s_2;
+        w.ln1_g = fp(lo[l].ln1_g);
+        w.ln1_b = fp(lo[l].ln1_b);
+        w.bqkv = fp(lo[l].bqkv);
+        w.bo = fp(lo[l].bo);
+        w.ln2_g = fp(lo[l].ln2_g);
+        w.ln2_b = fp(lo[l].ln2_b);
+        w.b1 = fp(lo[l].b1);
+        w.b2 = fp(lo[l].b2);
+    }
+    m->fin.lnf_g = fp(off_lnf_g);
+    m->fin.lnf_b = fp(off_lnf_b);
+    m->fin.w_score = fp(off_ws);
+    m->fin.b_score = fp(off_bs);
+    *out = m;
+    return ok();
+}
+
+void upr_model_destroy(upr_model* m) {
+    if (!m) return;
+    if (m->dev) (void)hipFree(m->dev);
+    delete m;
+}
+
+size_t upr_kv_cache_bytes(const upr_config* cfg, int64_t capacity_rows) {
+    if (check_config(cfg) != UPR_OK || capacity_rows < 0) return 0;
+    return (size_t)cfg->n_layers * 2 * cfg->n_heads * (size_t)capacity_rows * cfg->head_dim *
+           elem_size(*cfg);
+}
+
+int64_t upr_kv_cache_index(const upr_config* cfg, int64_t cap, int32_t layer, int32_t kv,
+                           int32_t head, int64_t row, int32_t e) {
+    if (check_config(cfg) != UPR_OK) return -1;
+    if (layer < 0 || layer >= cfg->n_layers || kv < 0 || kv > 1 || head < 0 ||
+        head >= cfg->n_heads || row < 0 || row >= cap || e < 0 || e >= cfg->head_dim)
+        return -1;
+    return ((((int64_t)layer * 2 + kv) * cfg->n_heads + head) * cap + row) * cfg->head_dim + e;
+}
+
+size_t upr_encode_workspace_bytes(const upr_model* m, const upr_segments* hist) {
+    if (!m) return 0;
+    int64_t first, last;
+    if (check_segments(hist, "hist", &first, &last) != UPR_OK) return 0;
+    return upr::plan_encode(m->cfg, first, last).bytes;
+}
+
+size_t upr_rank_workspace_bytes(const upr_model* m, const upr_segments* hist,
+                                const upr_segments* cand) {
+    if (!m) return 0;
+    int64_t hf, hl, cf, cl;
+    if (check_segments(hist, "hist", &hf, &hl) != UPR_OK) return 0;
+    if (check_segments(cand, "cand", &cf, &cl) != UPR_OK) return 0;
+    if (hist->num_users != cand->num_users) return 0;
+    return upr::plan_rank(m->cfg, cand->num_users, cand->offsets_host).bytes;
+}
+
+upr_status upr_encode_user(const upr_model* m, const void* hist_emb, const upr_segments* hist,
+                           const upr_kv_cache* cache, void* ws, size_t ws_bytes, void* stream) {
+    if (!m) return fail(UPR_ERR_NULL, "model is NULL");
+    int64_t first, last;
+    upr_status st = check_segments(hist, "hist", &first, &last);
+    if (st != UPR_OK) return st;
+    if (!cache) return fail(UPR_ERR_NULL, "cache is NULL");
+    if (last > first && !hist_emb) return fail(UPR_ERR_NULL, "hist_emb is NULL");
+    if (last > first && !cache->data) return fail(UPR_ERR_NULL, "cache data is NULL");
+    if (cache->capacity_rows < 0 || last > cache->capacity_rows)
+        return fail(UPR_ERR_CAPACITY, "history rows end at %lld, cache capacity is %lld",
+                    (long long)last, (long long)cache->capacity_rows);
+    const upr::EncodePlan p = upr::plan_encode(m->cfg, first, last);
+    st = check_workspace(ws, ws_bytes, p.bytes);
+    if (st != UPR_OK) return st;
+    if (p.rows == 0) return ok();
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* w = static_cast<char*>(ws);
+    st = m->cfg.dtype == UPR_BF16
+             ? upr::run_encode<upr::Bf16Types>(m, static_cast<const bf16*>(hist_emb), hist, cache,
+                                               p, w, s)
+             : upr::run_encode<upr::F32Types>(m, static_cast<const float*>(hist_emb), hist,
+                                              cache, p, w, s);
+    return st == UPR_OK ? ok() : st;
+}
+
+upr_status upr_rank_candidates(const upr_model* m, const upr_kv_cache* cache,
+                               const upr_segments* hist, const void* cand_emb,
+                               const upr_segments* cand, float* scores, void* ws,
+                               size_t ws_bytes, void* stream) {
+    if (!m) return fail(UPR_ERR_NULL, "model is NULL");
+    int64_t hf, hl, cf, cl;
+    upr_status st = check_segments(hist, "hist", &hf, &hl);
+    if (st != UPR_OK) return st;
+    st = check_segments(cand, "cand", &cf, &cl);
+    if (st != UPR_OK) return st;
+    if (hist->num_users != cand->num_users)
+        return fail(UPR_ERR_OFFSETS, "hist has %d users, cand has %d", hist->num_users,
+                    cand->num_users);
+    if (!cache) return fail(UPR_ERR_NULL, "cache is NULL");
+    if (cache->capacity_rows < 0 || hl > cache->capacity_rows)
+        return fail(UPR_ERR_CAPACITY, "history rows end at %lld, cache capacity is %lld",
+                    (long long)hl, (long long)cache->capacity_rows);
+    if (cl > cf) {
+        if (!cand_emb) return fail(UPR_ERR_NULL, "cand_emb is NULL");
+        if (!scores) return fail(UPR_ERR_NULL, "scores is NULL");
+        if (hl > hf && !cache->data) return fail(UPR_ERR_NULL, "cache data is NULL");
+    }
+    const upr::RankPlan p = upr::plan_rank(m->cfg, cand->num_users, cand->offsets_host);
+    st = check_workspace(ws, ws_bytes, p.bytes);
+    if (st != UPR_OK) return st;
+    if (p.rows == 0) return ok();
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* w = static_cast<char*>(ws);
+    st = m->cfg.dtype == UPR_BF16
+             ? upr::run_rank<upr::Bf16Types>(m, cache, hist, static_cast<const bf16*>(cand_emb),
+                                             cand, scores, p, w, s)
+             : upr::run_rank<upr::F32Types>(m, cache, hist, static_cast<const float*>(cand_emb),
+                                            cand, scores, p, w, s);
+    return st == UPR_OK ? ok() : st;
+}
+
+const char* upr_status_string(int32_t s) {
+    switch (s) {
+        case UPR_OK: return "ok";
+        case UPR_ERR_NULL: return "required pointer is NULL";
+        case UPR_ERR_CONFIG: return "unsupported model configuration";
+        case UPR_ERR_OFFSETS: return "malformed segment offsets";
+        case UPR_ERR_CAPACITY: return "history rows exceed cache capacity";
+        case UPR_ERR_WORKSPACE: return "workspace too small or misaligned";
+        case UPR_ERR_DTYPE: return "unknown dtype";
+        case UPR_ERR_HIP: return "HIP runtime error";
+        case UPR_ERR_WEIGHTS: return "weight blob size mismatch";
+        default: return "unknown status";
+    }
+}
+
+const char* upr_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

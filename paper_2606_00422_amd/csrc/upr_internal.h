@@ -1,0 +1,122 @@
+// Internal declarations shared by the library's host code and kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "upr.h"
+
+namespace upr {
+
+typedef __bf16 bf16;
+typedef _Float16 f16;
+
+// Storage types of the two model families.
+//   fp32 models: everything fp32.
+//   bf16 models: tokens, queries/keys/values, the cache and softmax
+//     probabilities are bf16; the operands of the projection GEMMs (LayerNorm
+//     outputs, attention output, FFN hidden, weights) are fp16, whose 11-bit
+//     significand holds every bf16 weight exactly and rounds activations 8x
+//     finer at the same MFMA rate; the residual stream and all accumulation
+//     are fp32.
+struct F32Types {
+    using kv = float;       // tokens, q/k/v, cache
+    using act = float;      // projection operands (activations and weights)
+};
+struct Bf16Types {
+    using kv = bf16;
+    using act = f16;
+};
+
+// Device copy of one layer's weights.  Matrices are [out, in] row-major in the
+// projection operand type; Wqkv stacks the rows of Wq, Wk and Wv ([3d, d]).
+// For bf16 models each matrix is stored multiplied by 2^k (an exact power of
+// two chosen so its largest magnitude lands in [2^14, 2^15)); the matching
+// s_* factor 2^-k undoes it on the fp32 accumulator.  Vectors are fp32.
+struct LayerWeights {
+    const void* Wqkv;
+    const void* Wo;
+    const void* W1;
+    const void* W2;
+    float s_qkv, s_o, s_1, s_2;
+    const float* ln1_g;
+    const float* ln1_b;
+    const float* bqkv;      // [3d]: bq, bk, bv
+    const float* bo;
+    const float* ln2_g;
+    const float* ln2_b;
+    const float* b1;
+    const float* b2;
+};
+
+struct FinalWeights {
+    const float* lnf_g;
+    const float* lnf_b;
+    const float* w_score;
+    const float* b_score;   // one value
+};
+
+constexpr int kMaxLayers = 64;
+
+// Epilogue modes of the projection GEMMs, out = A W^T + bias, then:
+enum EpiMode : int {
+    EPI_STORE = 0,      // out[m, n] (kv type); columns < scale_cols are multiplied by col_scale
+    EPI_GELU = 1,       // out[m, n] = gelu_tanh(.)  (projection operand type)
+    EPI_RESID = 2,      // resid[m, n] += .           (fp32, in place)
+    EPI_QKV_CACHE = 3,  // columns [0,d): query -> out (scaled); [d,2d): keys and
+                        // [2d,3d): values -> cache plane of the layer
+};
+
+struct Epilogue {
+    int mode;
+    float acc_scale;        // multiplies the accumulator first (weight scale)
+    const float* bias;      // [N]
+    void* out;              // EPI_STORE / EPI_GELU / EPI_QKV_CACHE (query part)
+    int64_t ldo;            // leading dimension of out (elements)
+    float* resid;           // EPI_RESID, leading dimension ldr
+    int64_t ldr;
+    float col_scale;        // applied to columns < scale_cols
+    int scale_cols;
+    // EPI_QKV_CACHE: cache plane of the layer and the absolute row of A's row 0
+    void* cache_k;          // &cache[l][0][0][0][0]
+    void* cache_v;          // &cache[l][1][0][0][0]
+    int64_t cache_cap;
+    int64_t row0;
+    int d_model;
+    int head_dim;
+};
+
+// ---------------------------------------------------------------------------
+// Launchers (all enqueue on `stream`; they return hipGetLastError()).
+// Row-wise kernels.
+// ---------------------------------------------------------------------------
+template <typename TKV>
+hipError_t launch_resid_init(const TKV* x, float* g, int64_t rows, int d, hipStream_t s);
+template <typename TA>
+hipError_t launch_layernorm(const float* g, TA* a, int64_t rows, int d, const float* gain,
+                            const float* shift, float eps, hipStream_t s);
+hipError_t launch_score_head(const float* g, float* scores, int64_t rows, int d,
+                             const FinalWeights& fw, float eps, hipStream_t s);
+
+// Reference-quality GEMM: out = A[M,K] W[N,K]^T + epilogue; A and W are of the
+// projection operand type TA, kv-typed epilogue outputs of type TKV.
+template <typename TA, typename TKV>
+hipError_t launch_gemm_simple(const TA* A, int64_t lda, const TA* W, int64_t M, int N, int K,
+                              const Epilogue& epi, hipStream_t s);
+
+// Reference-quality attention.  qkv / q rows are relative to the call's first
+// row `row0`; offsets are absolute.  Logits use exp2 with queries pre-scaled by
+// log2(e)/sqrt(D).  The output o is of the projection operand type TA.
+template <typename TKV, typename TA>
+hipError_t launch_attn_rank_simple(const TKV* qkv, TA* o, int64_t rows, int64_t row0, int H,
+                                   int D, const int32_t* cand_offsets,
+                                   const int32_t* hist_offsets, int num_users, const TKV* cache_k,
+                                   const TKV* cache_v, int64_t cache_cap, hipStream_t s);
+template <typename TKV, typename TA>
+hipError_t launch_attn_encode_simple(const TKV* q, TA* o, int64_t rows, int64_t row0, int H,
+                                     int D, const int32_t* hist_offsets, int num_users,
+                                     const TKV* cache_k, const TKV* cache_v, int64_t cache_cap,
+                                     hipStream_t s);
+
+}  // namespace upr

@@ -1,0 +1,99 @@
+// Workspace plans of encode and rank, and the launchers they dispatch to.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+
+#include "upr_internal.h"
+
+namespace upr {
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Candidates per work item of the MFMA ranking attention (one workgroup
+// handles this many candidates of one user for one head).
+constexpr int kRankAttnTile = 128;
+constexpr bool kHaveMfmaRankAttn = false;
+
+struct EncodePlan {
+    int64_t row0 = 0, rows = 0;
+    size_t off_g = 0, off_a = 0, off_q = 0, off_o = 0, off_h = 0;
+    size_t bytes = 0;
+};
+
+struct RankPlan {
+    int64_t row0 = 0, rows = 0;
+    size_t off_g = 0, off_a = 0, off_qkv = 0, off_o = 0, off_h = 0, off_work = 0;
+    int64_t work_items = 0;
+    int attn_tile = kRankAttnTile;
+    bool use_mfma_attn = false;
+    size_t bytes = 0;
+};
+
+inline size_t dtype_bytes(const upr_config& c) { return c.dtype == UPR_BF16 ? 2 : 4; }
+
+// Workspace of encode for history rows [first, last): fp32 residual stream,
+// then LayerNorm output, queries, attention output and FFN hidden (model dtype).
+inline EncodePlan plan_encode(const upr_config& c, int64_t first, int64_t last) {
+    EncodePlan p;
+    p.row0 = first;
+    p.rows = last - first;
+    if (p.rows <= 0) { p.rows = 0; return p; }
+    const size_t es = dtype_bytes(c), R = (size_t)p.rows, d = c.d_model, F = c.d_ff;
+    size_t o = 0;
+    p.off_g = o; o = align256(o + R * d * 4);
+    p.off_a = o; o = align256(o + R * d * es);
+    p.off_q = o; o = align256(o + R * d * es);
+    p.off_o = o; o = align256(o + R * d * es);
+    p.off_h = o; o = align256(o + R * F * es);
+    p.bytes = o;
+    return p;
+}
+
+// Workspace of rank for the candidate rows of `coffs` (host offsets):
+// residual, LayerNorm output, fused q|k|v rows, attention output, FFN hidden,
+// and (bf16 models) the attention work list.
+inline RankPlan plan_rank(const upr_config& c, int U, const int32_t* coffs) {
+    RankPlan p;
+    p.row0 = coffs[0];
+    p.rows = (int64_t)coffs[U] - coffs[0];
+    if (p.rows <= 0) { p.rows = 0; return p; }
+    const size_t es = dtype_bytes(c), R = (size_t)p.rows, d = c.d_model, F = c.d_ff;
+    p.use_mfma_attn = kHaveMfmaRankAttn && c.dtype == UPR_BF16 && c.head_dim == 64;
+    if (p.use_mfma_attn) {
+        int64_t items = 0;
+        for (int u = 0; u < U; ++u) {
+            const int64_t k = (int64_t)coffs[u + 1] - coffs[u];
+            items += (k + p.attn_tile - 1) / p.attn_tile;
+        }
+        p.work_items = items * c.n_heads;
+    }
+    size_t o = 0;
+    p.off_g = o; o = align256(o + R * d * 4);
+    p.off_a = o; o = align256(o + R * d * es);
+    p.off_qkv = o; o = align256(o + R * 3 * d * es);
+    p.off_o = o; o = align256(o + R * d * es);
+    p.off_h = o; o = align256(o + R * F * es);
+    p.off_work = o; o = align256(o + (size_t)p.work_items * 4 * sizeof(int32_t));
+    p.bytes = o;
+    return p;
+}
+
+// Projection GEMM, out = A[M,K] W[N,K]^T + epilogue: fp32 models use the
+// reference FMA kernel, bf16 models the fp16 MFMA kernel.
+template <typename TA, typename TKV>
+hipError_t launch_gemm(const TA* A, int64_t lda, const TA* W, int64_t M, int N, int K,
+                       const Epilogue& epi, hipStream_t s);
+
+// Work list of the MFMA ranking attention: entries (user, head, first
+// candidate row, candidate count), heaviest users first.
+hipError_t launch_rank_worklist(const int32_t* cand_offsets, const int32_t* hist_offsets, int U,
+                                int H, int tile, int32_t* work, int64_t items, hipStream_t s);
+
+// MFMA ranking attention (bf16 queries/cache, head_dim 64), fp16 output.
+hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
+                            const int32_t* cand_offsets, const int32_t* hist_offsets,
+                            const int32_t* work, int64_t items, int tile, const bf16* cache_k,
+                            const bf16* cache_v, int64_t cache_cap, hipStream_t s);
+
+}  // namespace upr

@@ -1,0 +1,244 @@
+"""ctypes binding of libupr.so (include/upr.h), argument marshalling only.
+
+The functions keep the C names.  Pointers are passed as Python ints (device
+pointers from ``tensor.data_ptr()``, host pointers from numpy arrays); the
+``*_t`` helpers below accept torch tensors / numpy arrays and check dtypes,
+devices and contiguity before calling into the library.  Every compute step
+runs in the library's HIP kernels; there is no Python or CPU fallback: if the
+shared library is missing, loading fails with an error.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libupr.so")
+
+UPR_OK, UPR_ERR_NULL, UPR_ERR_CONFIG, UPR_ERR_OFFSETS, UPR_ERR_CAPACITY = 0, 1, 2, 3, 4
+UPR_ERR_WORKSPACE, UPR_ERR_DTYPE, UPR_ERR_HIP, UPR_ERR_WEIGHTS = 5, 6, 7, 8
+UPR_F32, UPR_BF16 = 0, 1
+
+# Every symbol include/upr.h declares.
+EXPORTS = (
+    "upr_weights_count", "upr_model_create", "upr_model_destroy", "upr_kv_cache_bytes",
+    "upr_kv_cache_index", "upr_encode_workspace_bytes", "upr_rank_workspace_bytes",
+    "upr_encode_user", "upr_rank_candidates", "upr_status_string", "upr_last_error",
+)
+
+
+class upr_config(ctypes.Structure):
+    _fields_ = [("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("n_layers", ctypes.c_int32),
+                ("d_ff", ctypes.c_int32), ("dtype", ctypes.c_int32), ("ln_eps", ctypes.c_float)]
+
+
+class upr_segments(ctypes.Structure):
+    _fields_ = [("num_users", ctypes.c_int32), ("offsets_host", ctypes.c_void_p),
+                ("offsets_dev", ctypes.c_void_p)]
+
+
+class upr_kv_cache(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("capacity_rows", ctypes.c_int64)]
+
+
+class UprError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"upr status {status}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load the shared library (once) and declare every signature."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with paper_2606_00422_amd/build.py "
+                          "(or __graft_entry__.build())")
+    lib = ctypes.CDLL(path)
+    P, I32, I64, SZ, VP = ctypes.POINTER, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p
+    cfgp, segp, cachep = P(upr_config), P(upr_segments), P(upr_kv_cache)
+    sig = {
+        "upr_weights_count": (I64, [cfgp]),
+        "upr_model_create": (I32, [cfgp, VP, I64, P(VP)]),
+        "upr_model_destroy": (None, [VP]),
+        "upr_kv_cache_bytes": (SZ, [cfgp, I64]),
+        "upr_kv_cache_index": (I64, [cfgp, I64, I32, I32, I32, I64, I32]),
+        "upr_encode_workspace_bytes": (SZ, [VP, segp]),
+        "upr_rank_workspace_bytes": (SZ, [VP, segp, segp]),
+        "upr_encode_user": (I32, [VP, VP, segp, cachep, VP, SZ, VP]),
+        "upr_rank_candidates": (I32, [VP, cachep, segp, VP, segp, VP, VP, SZ, VP]),
+        "upr_status_string": (ctypes.c_char_p, [I32]),
+        "upr_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != UPR_OK:
+        lib = load()
+        raise UprError(status, lib.upr_last_error().decode() or
+                       lib.upr_status_string(status).decode())
+
+
+# ---------------------------------------------------------------------------
+# The C calls, same names, plain arguments
+# ---------------------------------------------------------------------------
+
+def make_config(d_model, n_heads, n_layers, d_ff, dtype, ln_eps=1e-5) -> upr_config:
+    if d_model % n_heads:
+        raise ValueError("d_model must be a multiple of n_heads")
+    return upr_config(d_model, n_heads, d_model // n_heads, n_layers, d_ff,
+                      UPR_BF16 if dtype in ("bf16", UPR_BF16) else UPR_F32, ln_eps)
+
+
+def upr_weights_count(cfg: upr_config) -> int:
+    return int(load().upr_weights_count(ctypes.byref(cfg)))
+
+
+def upr_model_create(cfg: upr_config, weights: np.ndarray) -> int:
+    w = np.ascontiguousarray(weights, dtype=np.float32)
+    out = ctypes.c_void_p()
+    _check(load().upr_model_create(ctypes.byref(cfg), w.ctypes.data, w.size, ctypes.byref(out)))
+    return int(out.value)
+
+
+def upr_model_destroy(model: int) -> None:
+    load().upr_model_destroy(model)
+
+
+def upr_kv_cache_bytes(cfg: upr_config, capacity_rows: int) -> int:
+    return int(load().upr_kv_cache_bytes(ctypes.byref(cfg), capacity_rows))
+
+
+def upr_kv_cache_index(cfg, capacity_rows, layer, kv, head, row, e) -> int:
+    return int(load().upr_kv_cache_index(ctypes.byref(cfg), capacity_rows, layer, kv, head, row, e))
+
+
+def upr_encode_workspace_bytes(model: int, hist: upr_segments) -> int:
+    return int(load().upr_encode_workspace_bytes(model, ctypes.byref(hist)))
+
+
+def upr_rank_workspace_bytes(model: int, hist: upr_segments, cand: upr_segments) -> int:
+    return int(load().upr_rank_workspace_bytes(model, ctypes.byref(hist), ctypes.byref(cand)))
+
+
+def upr_encode_user(model, hist_emb_ptr, hist: upr_segments, cache: upr_kv_cache,
+                    ws_ptr, ws_bytes, stream) -> None:
+    _check(load().upr_encode_user(model, hist_emb_ptr, ctypes.byref(hist), ctypes.byref(cache),
+                                  ws_ptr, ws_bytes, stream))
+
+
+def upr_rank_candidates(model, cache: upr_kv_cache, hist: upr_segments, cand_emb_ptr,
+                        cand: upr_segments, scores_ptr, ws_ptr, ws_bytes, stream) -> None:
+    _check(load().upr_rank_candidates(model, ctypes.byref(cache), ctypes.byref(hist), cand_emb_ptr,
+                                      ctypes.byref(cand), scores_ptr, ws_ptr, ws_bytes, stream))
+
+
+def upr_status_string(status: int) -> str:
+    return load().upr_status_string(status).decode()
+
+
+def upr_last_error() -> str:
+    return load().upr_last_error().decode()
+
+
+# ---------------------------------------------------------------------------
+# Marshalling helpers for torch device tensors (torch supplies memory/streams)
+# ---------------------------------------------------------------------------
+
+def segments(offsets_host: np.ndarray, offsets_dev=None) -> upr_segments:
+    """Descriptor over a host int32 offsets array and its device copy (a torch
+    int32 tensor).  The caller keeps both alive for the duration of the call."""
+    if offsets_host.dtype != np.int32 or not offsets_host.flags["C_CONTIGUOUS"]:
+        raise TypeError("offsets_host must be a contiguous int32 numpy array")
+    dev = 0
+    if offsets_dev is not None:
+        _check_tensor(offsets_dev, "offsets_dev", "int32")
+        dev = offsets_dev.data_ptr()
+    return upr_segments(int(offsets_host.shape[0] - 1), offsets_host.ctypes.data, dev)
+
+
+def _check_tensor(t, name, dtype=None):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise TypeError(f"{name} must be contiguous")
+    if dtype is not None and str(t.dtype) != f"torch.{dtype}":
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+def current_stream() -> int:
+    import torch
+    return int(torch.cuda.current_stream().cuda_stream)
+
+
+class Model:
+    """A created model plus the tensor-level encode/rank calls."""
+
+    def __init__(self, cfg: upr_config, weights: np.ndarray):
+        self.cfg = cfg
+        self.handle = upr_model_create(cfg, weights)
+        self.torch_dtype = "bfloat16" if cfg.dtype == UPR_BF16 else "float32"
+
+    def close(self):
+        if self.handle:
+            upr_model_destroy(self.handle)
+            self.handle = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def new_cache(self, capacity_rows: int):
+        import torch
+        dt = torch.bfloat16 if self.cfg.dtype == UPR_BF16 else torch.float32
+        c = self.cfg
+        cache = torch.zeros((c.n_layers, 2, c.n_heads, capacity_rows, c.head_dim), dtype=dt,
+                            device="cuda")
+        assert cache.numel() * cache.element_size() == upr_kv_cache_bytes(c, capacity_rows)
+        return cache
+
+    def workspace(self, nbytes: int):
+        import torch
+        return torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
+
+    def encode(self, hist_emb, hist_off_host, hist_off_dev, cache, ws=None, stream=None):
+        _check_tensor(hist_emb, "hist_emb", self.torch_dtype)
+        _check_tensor(cache, "cache", self.torch_dtype)
+        seg = segments(hist_off_host, hist_off_dev)
+        need = upr_encode_workspace_bytes(self.handle, seg)
+        if ws is None:
+            ws = self.workspace(need)
+        kv = upr_kv_cache(cache.data_ptr(), cache.shape[3])
+        upr_encode_user(self.handle, hist_emb.data_ptr(), seg, kv, ws.data_ptr(), ws.numel(),
+                        current_stream() if stream is None else stream)
+        return ws
+
+    def rank(self, cache, hist_off_host, hist_off_dev, cand_emb, cand_off_host, cand_off_dev,
+             scores, ws=None, stream=None):
+        _check_tensor(cand_emb, "cand_emb", self.torch_dtype)
+        _check_tensor(cache, "cache", self.torch_dtype)
+        _check_tensor(scores, "scores", "float32")
+        hs = segments(hist_off_host, hist_off_dev)
+        cs = segments(cand_off_host, cand_off_dev)
+        need = upr_rank_workspace_bytes(self.handle, hs, cs)
+        if ws is None:
+            ws = self.workspace(need)
+        kv = upr_kv_cache(cache.data_ptr(), cache.shape[3])
+        upr_rank_candidates(self.handle, kv, hs, cand_emb.data_ptr(), cs, scores.data_ptr(),
+                            ws.data_ptr(), ws.numel(), current_stream() if stream is None else stream)
+        return ws

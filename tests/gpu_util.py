@@ -1,0 +1,131 @@
+"""Helpers shared by the GPU tests: run the library on seeded inputs and
+compare with the oracle under the stated rules."""
+import sys
+
+import numpy as np
+
+from paper_2606_00422_amd import upr
+
+# Comparison rules for bf16 inputs with fp32 accumulation: elementwise
+# |gpu - oracle| <= ATOL + RTOL * |oracle|, and every pair of one user's
+# candidates whose oracle scores differ by more than ORDER_GAP keeps its order.
+ATOL, RTOL, ORDER_GAP = 2e-2, 1e-2, 5e-2
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+class GpuRun:
+    """Device buffers of one problem plus a model; encode/rank through the C ABI."""
+
+    def __init__(self, inp, capacity_rows=None):
+        import torch
+        self.inp = inp
+        self.cfg = upr.make_config(inp.d, inp.H, inp.L, inp.F, inp.dtype)
+        self.model = upr.Model(self.cfg, inp.weights)
+        self.tdt = torch.bfloat16 if inp.dtype == "bf16" else torch.float32
+        dev = "cuda"
+        self.X = torch.from_numpy(inp.hist_emb).to(dev).to(self.tdt)
+        self.C = torch.from_numpy(inp.cand_emb).to(dev).to(self.tdt)
+        self.hoff = np.ascontiguousarray(inp.hist_offsets, dtype=np.int32)
+        self.coff = np.ascontiguousarray(inp.cand_offsets, dtype=np.int32)
+        self.hoff_d = torch.from_numpy(self.hoff).to(dev)
+        self.coff_d = torch.from_numpy(self.coff).to(dev)
+        cap = int(self.hoff[-1]) if capacity_rows is None else capacity_rows
+        self.cap = max(cap, 1)
+        self.cache = self.model.new_cache(self.cap)
+        self.scores = torch.full((max(int(self.coff[-1]), 1),), float("nan"),
+                                 dtype=torch.float32, device=dev)
+
+    def encode(self, hoff=None):
+        hoff = self.hoff if hoff is None else hoff
+        import torch
+        hd = torch.from_numpy(hoff).to("cuda")
+        self.model.encode(self.X, hoff, hd, self.cache)
+
+    def rank(self, hoff=None, coff=None, scores=None):
+        import torch
+        hoff = self.hoff if hoff is None else hoff
+        coff = self.coff if coff is None else coff
+        hd = torch.from_numpy(hoff).to("cuda")
+        cd = torch.from_numpy(coff).to("cuda")
+        out = self.scores if scores is None else scores
+        self.model.rank(self.cache, hoff, hd, self.C, coff, cd, out)
+        return out
+
+    def scores_np(self):
+        import torch
+        torch.cuda.synchronize()
+        return self.scores.cpu().numpy().astype(np.float64)
+
+    def cache_np(self):
+        import torch
+        torch.cuda.synchronize()
+        return self.cache.float().cpu().numpy().astype(np.float64)
+
+
+def assert_scores_match(gpu, ref, label="", scale=1.0):
+    """Scores within scale * (ATOL + RTOL |oracle|).  scale is 1 for every
+    workload; the sharp-logit stress variant multiplies the query weights, and
+    with them the logit error of bf16 queries and keys, by 4 and passes 4."""
+    gpu = np.asarray(gpu, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert np.all(np.isfinite(gpu)), f"{label}: non-finite GPU scores"
+    err = np.abs(gpu - ref)
+    bound = scale * (ATOL + RTOL * np.abs(ref))
+    bad = np.flatnonzero(err > bound)
+    worst = int(np.argmax(err - bound)) if err.size else 0
+    msg = (f"{label}: {bad.size}/{err.size} scores outside {scale}*({ATOL} + {RTOL}|o|); max abs err "
+           f"{err.max() if err.size else 0:.3e}; worst row {worst}: gpu {gpu[worst]:.5f} "
+           f"oracle {ref[worst]:.5f}")
+    assert bad.size == 0, msg
+    return float(err.max()) if err.size else 0.0
+
+
+def assert_order_kept(gpu, ref, groups, label=""):
+    """For every group (array of row indices of one user): any pair with
+    ref_i - ref_j > ORDER_GAP must have gpu_i > gpu_j."""
+    for rows in groups:
+        if len(rows) < 2:
+            continue
+        r = np.asarray(ref)[rows]
+        g = np.asarray(gpu)[rows]
+        order = np.argsort(r, kind="stable")
+        r_sorted, g_sorted = r[order], g[order]
+        prefmax = np.maximum.accumulate(g_sorted)
+        cnt = np.searchsorted(r_sorted, r_sorted - ORDER_GAP, side="left")
+        for i in range(len(rows)):
+            c = cnt[i]
+            if c > 0:
+                assert g_sorted[i] > prefmax[c - 1], (
+                    f"{label}: order broken for a pair with oracle gap > {ORDER_GAP}")
+
+
+def cache_atol(layer):
+    """Absolute cache tolerance of layer `layer`.
+
+    Layer 0 keys/values carry two bf16 roundings (the LayerNorm output and
+    the stored value), so the score tolerance's 2e-2 covers them.  Every
+    further layer inherits one more round of rounded activations (attention
+    output, FFN hidden, next LayerNorm output) through the residual stream,
+    so the budget grows by the same amount per layer.
+    """
+    return ATOL * (layer + 1)
+
+
+def assert_cache_match(gpu_cache, ref_cache, rows, label=""):
+    """Elementwise cache comparison at identical (layer, kv, head, row, e);
+    any mis-indexed row shows up as an O(1) error."""
+    worst = 0.0
+    for l in range(gpu_cache.shape[0]):
+        g = gpu_cache[l][:, :, rows, :]
+        o = ref_cache[l][:, :, rows, :]
+        err = np.abs(g - o)
+        bound = cache_atol(l) + RTOL * np.abs(o)
+        assert np.all(err <= bound), (
+            f"{label}: cache layer {l} mismatch, max abs err {err.max():.3e} "
+            f"at {np.unravel_index(np.argmax(err - bound), err.shape)} (bound {cache_atol(l)})")
+        worst = max(worst, float(err.max()))
+    return worst

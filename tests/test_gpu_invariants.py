@@ -1,0 +1,149 @@
+"""GPU-side invariants of the method, through the C ABI.
+
+Candidates never see each other (Sec. 3, attention pattern; KV-cache
+section: scores independent of batch composition), so on the GPU:
+permuting candidates permutes scores bit-exactly, a single-user call on a
+sub-range of the packed buffers reproduces the batched scores bit-exactly,
+and repeated runs are bit-identical.  Validation errors leave outputs
+untouched.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+
+from paper_2606_00422_amd import upr
+from synth import make_inputs, make_workload
+from tests.gpu_util import GpuRun, assert_scores_match, say
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+
+def _inp():
+    return make_inputs([130, 0, 257, 64], [300, 17, 129, 1], 256, 4, 2, 512, dtype="bf16",
+                       seed=21, variant="perturbed")
+
+
+def test_candidate_permutation_is_bit_exact():
+    import torch
+    inp = _inp()
+    say("[gpu] permutation")
+    base = GpuRun(inp)
+    base.encode()
+    base.rank()
+    s0 = base.scores_np()
+    rng = np.random.default_rng(0)
+    co = inp.cand_offsets
+    perm = np.concatenate([co[u] + rng.permutation(co[u + 1] - co[u]) for u in range(inp.U)])
+    inp2 = _inp()
+    inp2.cand_emb = inp.cand_emb[perm]
+    run = GpuRun(inp2)
+    run.encode()
+    run.rank()
+    s1 = run.scores_np()
+    assert np.array_equal(s1[: co[-1]], s0[perm])
+
+
+def test_sub_range_single_user_calls_match_batch_bit_exactly():
+    inp = _inp()
+    say("[gpu] single-user sub-range calls")
+    run = GpuRun(inp)
+    run.encode()
+    run.rank()
+    batch = run.scores_np().copy()
+    import torch
+    ho, co = inp.hist_offsets, inp.cand_offsets
+    for u in range(inp.U):
+        run.scores.fill_(float("nan"))
+        hoff = np.array([ho[u], ho[u + 1]], np.int32)
+        coff = np.array([co[u], co[u + 1]], np.int32)
+        run.rank(hoff=hoff, coff=coff)
+        s = run.scores_np()
+        assert np.array_equal(s[co[u]:co[u + 1]], batch[co[u]:co[u + 1]]), f"user {u}"
+        others = np.ones(s.shape[0], bool)
+        others[co[u]:co[u + 1]] = False
+        assert np.all(np.isnan(s[others])), "rows outside the call were written"
+
+
+def test_sub_range_encode_matches_batch_encode():
+    inp = _inp()
+    say("[gpu] per-user encode")
+    a = GpuRun(inp)
+    a.encode()
+    ca = a.cache_np()
+    b = GpuRun(inp)
+    ho = inp.hist_offsets
+    for u in range(inp.U):
+        b.encode(hoff=np.array([ho[u], ho[u + 1]], np.int32))
+    cb = b.cache_np()
+    assert np.array_equal(ca, cb)
+
+
+def test_repeated_runs_are_bit_identical():
+    inp = make_workload("u16_n256_k1000", seed=3)
+    say("[gpu] determinism")
+    run = GpuRun(inp)
+    run.encode()
+    c0 = run.cache_np()
+    run.rank()
+    s0 = run.scores_np().copy()
+    for _ in range(2):
+        run.encode()
+        run.rank()
+        assert np.array_equal(run.scores_np(), s0)
+        assert np.array_equal(run.cache_np(), c0)
+
+
+def test_empty_history_user_scores_match_oracle():
+    inp = make_inputs([0, 0], [40, 3], 128, 2, 2, 256, dtype="bf16", seed=4, variant="perturbed")
+    say("[gpu] empty histories")
+    run = GpuRun(inp, capacity_rows=1)
+    run.encode()
+    run.rank()
+    s = run.scores_np()
+    cache = np.zeros((2, 2, 2, 1, 64))
+    ref = oracle.rank(inp.weights, inp.d, inp.H, inp.L, inp.F, cache, inp.hist_offsets,
+                      inp.cand_emb, inp.cand_offsets)
+    assert_scores_match(s[:43], ref, "empty histories")
+
+
+@pytest.mark.parametrize("what", ["decreasing", "capacity", "workspace", "users", "null_scores"])
+def test_validation_errors_leave_outputs_untouched(what):
+    import torch
+    inp = make_inputs([20, 30], [10, 12], 128, 2, 1, 256, dtype="bf16", seed=6)
+    run = GpuRun(inp)
+    run.encode()
+    run.scores.fill_(123.0)
+    cache_before = run.cache.clone()
+    hs = upr.segments(run.hoff, run.hoff_d)
+    cs = upr.segments(run.coff, run.coff_d)
+    need = upr.upr_rank_workspace_bytes(run.model.handle, hs, cs)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    kv = upr.upr_kv_cache(run.cache.data_ptr(), run.cap)
+    scores_ptr = run.scores.data_ptr()
+    ws_bytes = need
+    if what == "decreasing":
+        bad = np.array([0, 12, 10], np.int32)
+        cs = upr.segments(bad, run.coff_d)
+        code = upr.UPR_ERR_OFFSETS
+    elif what == "capacity":
+        kv = upr.upr_kv_cache(run.cache.data_ptr(), 49)
+        code = upr.UPR_ERR_CAPACITY
+    elif what == "workspace":
+        ws_bytes = need - 1
+        code = upr.UPR_ERR_WORKSPACE
+    elif what == "users":
+        one = np.array([0, 22], np.int32)
+        cs = upr.segments(one, run.coff_d)
+        code = upr.UPR_ERR_OFFSETS
+    else:
+        scores_ptr = 0
+        code = upr.UPR_ERR_NULL
+    with pytest.raises(upr.UprError) as ei:
+        upr.upr_rank_candidates(run.model.handle, kv, hs, run.C.data_ptr(), cs, scores_ptr,
+                                ws.data_ptr(), ws_bytes, upr.current_stream())
+    assert ei.value.status == code
+    torch.cuda.synchronize()
+    assert torch.all(run.scores == 123.0)
+    assert torch.equal(run.cache, cache_before)

@@ -1,0 +1,244 @@
+"""Benchmark: candidate scores/s of one batched rank call on one MI355X.
+
+One step = one upr_rank_candidates call over the whole workload (every layer's
+LayerNorm, Q/K/V projection, candidate cross-attention over the cached
+history, output projection, FFN, and the score head), with inputs and the
+cache already resident in HBM.  The cache comes from one prior
+upr_encode_user call, timed separately.
+
+Prints one JSON line.  Besides the contract fields it carries:
+  roofline      - the dominant kernel: algorithmic work per launch / its mean
+                  duration (HIP events on the call's stream, from a second,
+                  profiled pass over the same steps), against MI355X's peak;
+  cpu_baseline  - the CPU oracle ranking a bounded sample of the same
+                  workload on this host's cores;
+  path_mfma_frac, p50/p90 single-user latency, encode time, per-kernel times.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from synth import WORKLOADS, make_workload  # noqa: E402
+
+PEAK_MFMA_TFLOPS = 2500.0     # MI355X dense bf16 / fp16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def kernel_work(inp):
+    """Algorithmic FLOPs per launch of each rank kernel, and bytes for the
+    memory-bound ones (one launch = one layer's pass over all candidates)."""
+    d, F, H = inp.d, inp.F, inp.H
+    R = int(inp.cand_offsets[-1] - inp.cand_offsets[0])
+    n = inp.hist_lens
+    k = inp.cand_lens
+    es = 2 if inp.dtype == "bf16" else 4
+    attn_pairs = int(np.sum(k * (n + 1)))
+    return {
+        "rank.gemm_qkv": ("mfma", 2.0 * R * 3 * d * d),
+        "rank.gemm_o": ("mfma", 2.0 * R * d * d),
+        "rank.gemm_up": ("mfma", 2.0 * R * F * d),
+        "rank.gemm_down": ("mfma", 2.0 * R * d * F),
+        # q.k and p.v over the history plus the candidate's own key
+        "rank.attn": ("mfma", 4.0 * d * attn_pairs),
+        # read the fp32 residual, write the normalised row
+        "rank.ln1": ("hbm", R * d * (4.0 + es)),
+        "rank.ln2": ("hbm", R * d * (4.0 + es)),
+        "rank.score_head": ("hbm", R * d * 4.0 + R * 4.0),
+        "rank.resid_init": ("hbm", R * d * (es + 4.0)),
+    }
+
+
+def path_flops(inp):
+    d, F, L = inp.d, inp.F, inp.L
+    R = float(inp.cand_offsets[-1] - inp.cand_offsets[0])
+    pairs = float(np.sum(inp.cand_lens * (inp.hist_lens + 1)))
+    return L * (R * (8 * d * d + 4 * d * F) + 4 * d * pairs) + 2 * d * R
+
+
+def cpu_baseline(inp, budget_s=12.0):
+    """Oracle rank on a bounded sample of users (its cache from oracle.encode,
+    untimed: encoding is the step before ranking)."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        blas = ",".join(sorted({i.get("internal_api", "?") for i in threadpool_info()}))
+    except Exception:
+        threads, blas = os.cpu_count() or 1, "unknown"
+    done_users, cands, t_rank = [], 0, 0.0
+    order = np.argsort(-inp.cand_lens, kind="stable")        # typical users first
+    order = order[len(order) // 2:].tolist() + order[: len(order) // 2].tolist()
+    for u in order:
+        cache = oracle.encode(inp.weights, inp.d, inp.H, inp.L, inp.F, inp.hist_emb,
+                              inp.hist_offsets, users=[u])
+        t0 = time.perf_counter()
+        oracle.rank(inp.weights, inp.d, inp.H, inp.L, inp.F, cache, inp.hist_offsets,
+                    inp.cand_emb, inp.cand_offsets, users=[u])
+        t_rank += time.perf_counter() - t0
+        done_users.append(int(u))
+        cands += int(inp.cand_lens[u])
+        if t_rank >= budget_s:
+            break
+    return {"value": cands / t_rank, "unit": "candidate scores/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"oracle.rank (numpy float64, BLAS {blas}) over {len(done_users)} of "
+                      f"{inp.U} users ({cands} candidates), {t_rank:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="u64_n1024_k2000", choices=sorted(WORKLOADS))
+    ap.add_argument("--user-reps", type=int, default=3, help="reps of the per-user latency pass")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this path has no "
+              "multi-GPU mode; per-GPU work is independent by user.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_00422_amd import upr
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    inp = make_workload(args.workload, seed=args.seed)
+    cfg = upr.make_config(inp.d, inp.H, inp.L, inp.F, inp.dtype)
+    model = upr.Model(cfg, inp.weights)
+    tdt = torch.bfloat16 if inp.dtype == "bf16" else torch.float32
+    X = torch.from_numpy(inp.hist_emb).cuda().to(tdt)
+    C = torch.from_numpy(inp.cand_emb).cuda().to(tdt)
+    hoff = np.ascontiguousarray(inp.hist_offsets, np.int32)
+    coff = np.ascontiguousarray(inp.cand_offsets, np.int32)
+    hoff_d = torch.from_numpy(hoff).cuda()
+    coff_d = torch.from_numpy(coff).cuda()
+    T, Kc = int(hoff[-1]), int(coff[-1])
+    cache = model.new_cache(max(T, 1))
+    scores = torch.empty(max(Kc, 1), dtype=torch.float32, device="cuda")
+    hs, cs = upr.segments(hoff, hoff_d), upr.segments(coff, coff_d)
+    ws = model.workspace(max(upr.upr_encode_workspace_bytes(model.handle, hs),
+                             upr.upr_rank_workspace_bytes(model.handle, hs, cs)))
+    stream = upr.current_stream()
+    kv = upr.upr_kv_cache(cache.data_ptr(), cache.shape[3])
+
+    def encode():
+        upr.upr_encode_user(model.handle, X.data_ptr(), hs, kv, ws.data_ptr(), ws.numel(), stream)
+
+    def rank(h=hs, c=cs):
+        upr.upr_rank_candidates(model.handle, kv, h, C.data_ptr(), c, scores.data_ptr(),
+                                ws.data_ptr(), ws.numel(), stream)
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    encode()
+    torch.cuda.synchronize()
+    e0, e1 = ev(), ev()
+    e0.record()
+    encode()
+    e1.record()
+    torch.cuda.synchronize()
+    encode_ms = e0.elapsed_time(e1)
+
+    for _ in range(args.warmup):
+        rank()
+    torch.cuda.synchronize()
+    # timed region (no per-kernel events inside)
+    e0, e1 = ev(), ev()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        rank()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    assert bool(torch.isfinite(scores[:Kc]).all()), "non-finite scores"
+
+    # profiled pass over the same steps: per-kernel HIP events on the stream
+    upr.upr_profile_enable(True)
+    for _ in range(args.steps):
+        rank()
+    torch.cuda.synchronize()
+    prof = upr.upr_profile_read()
+    upr.upr_profile_enable(False)
+
+    work = kernel_work(inp)
+    kernels = {}
+    for name, (launches, total) in sorted(prof.items()):
+        avg = total / launches
+        entry = {"launches_per_step": launches / args.steps, "avg_ms": round(avg, 5)}
+        if name in work:
+            bound, amount = work[name]
+            if bound == "mfma":
+                entry["tflops"] = round(amount / (avg * 1e-3) / 1e12, 2)
+            else:
+                entry["gbs"] = round(amount / (avg * 1e-3) / 1e9, 1)
+        kernels[name] = entry
+    dom = max((n for n in prof if n in work), key=lambda n: prof[n][1])
+    bound, amount = work[dom]
+    avg_s = prof[dom][1] / prof[dom][0] * 1e-3
+    if bound == "mfma":
+        achieved = amount / avg_s / 1e12
+        roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
+                "peak": PEAK_MFMA_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_MFMA_TFLOPS, 4), "traffic": None}
+    else:
+        achieved = amount / avg_s / 1e9
+        roof = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
+                "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+
+    # single-user calls (sub-range of the packed buffers), per-call latency
+    lat = []
+    for _ in range(args.user_reps):
+        for u in range(inp.U):
+            h1 = upr.segments(np.ascontiguousarray(hoff[u:u + 2]), hoff_d[u:u + 2])
+            c1 = upr.segments(np.ascontiguousarray(coff[u:u + 2]), coff_d[u:u + 2])
+            a, b = ev(), ev()
+            a.record()
+            rank(h1, c1)
+            b.record()
+            torch.cuda.synchronize()
+            lat.append(a.elapsed_time(b))
+    lat = np.array(lat)
+
+    flops = path_flops(inp)
+    out = {
+        "metric": "candidate scores/sec (1 GPU)",
+        "value": round(Kc / (ms * 1e-3), 1),
+        "unit": "candidate scores/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16+fp16" if inp.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "users": inp.U,
+                   "history_rows": T, "candidate_rows": Kc, "d_model": inp.d,
+                   "heads": inp.H, "layers": inp.L, "d_ff": inp.F},
+        "path_tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+        "path_mfma_frac": round(flops / (ms * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
+        "user_latency_ms": {"p50": round(float(np.percentile(lat, 50)), 4),
+                            "p90": round(float(np.percentile(lat, 90)), 4),
+                            "calls": int(lat.size)},
+        "encode_ms": round(encode_ms, 3),
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(inp)
+    print(json.dumps(out), flush=True)
+    model.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -56,10 +56,18 @@ typedef enum { UPR_F32 = 0, UPR_BF16 = 1 } upr_dtype;
 
 /* Model shape.  Supported: head_dim in {32, 64}; d_model = n_heads*head_dim,
  * a multiple of 64 and at most 1024; d_ff a multiple of 64 and at most 8192;
- * 1 <= n_layers <= 64.  dtype selects the storage/arithmetic type of
- * activations, weights, tokens and cache: UPR_F32 computes in fp32
- * throughout; UPR_BF16 stores bf16 and accumulates every contraction,
- * normalisation and softmax in fp32.  ln_eps is the LayerNorm epsilon. */
+ * 1 <= n_layers <= 64.  dtype selects the storage type of tokens and cache
+ * and the arithmetic of the model:
+ *   UPR_F32:  fp32 throughout.
+ *   UPR_BF16: tokens, the K/V cache, queries/keys/values and softmax
+ *             probabilities are bf16 (attention contractions are bf16 MFMA);
+ *             the operands of the projection GEMMs (LayerNorm outputs,
+ *             attention output, FFN hidden, weights) are fp16 (fp16 MFMA,
+ *             same peak rate, 3 more significand bits); the residual stream,
+ *             normalisation statistics, softmax and every accumulation are
+ *             fp32.  Activations entering the projections must stay within
+ *             the fp16 range (|x| < 65504).
+ * ln_eps is the LayerNorm epsilon. */
 typedef struct {
     int32_t d_model;
     int32_t n_heads;
@@ -99,8 +107,11 @@ typedef struct {
 int64_t upr_weights_count(const upr_config* cfg);
 
 /* Create a model: copies the host blob (weights_count floats) to device
- * memory.  For UPR_BF16 the matrices are rounded to bf16 (nearest, ties to
- * even) and the vectors (gains, shifts, biases, score weights) kept in fp32.
+ * memory.  For UPR_BF16 every matrix value is rounded to bf16 (nearest, ties
+ * to even) -- the model's weights are bf16 -- and stored as fp16 after an
+ * exact per-matrix power-of-two scaling (undone in fp32 after each GEMM), so
+ * every bf16 weight within 2^29 of its matrix's largest magnitude is kept
+ * exactly.  Vectors (gains, shifts, biases, score weights) stay fp32.
  * This is the only call that allocates device memory.  The blob may be freed
  * after return.  *out is set only on UPR_OK. */
 upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
@@ -152,6 +163,24 @@ upr_status upr_rank_candidates(const upr_model* model, const upr_kv_cache* cache
                                const upr_segments* hist, const void* cand_emb,
                                const upr_segments* cand, float* scores,
                                void* ws, size_t ws_bytes, void* stream);
+
+/* Diagnostics: per-kernel timing with HIP events.  While enabled, encode and
+ * rank record a pair of hipEvents on the call's stream around every kernel
+ * they launch, labelled with the kernel's name (e.g. "rank.attn").
+ * upr_profile_read waits for those events and reports, per name, the number
+ * of launches and their summed duration since profiling was last enabled;
+ * it returns the number of names (writing at most max_entries to out, which
+ * may be NULL).  upr_profile_enable(0/1) discards what was recorded.  The
+ * events are created on first use and reused; this path is for measurement,
+ * not for serving. */
+typedef struct {
+    char name[48];
+    int64_t launches;
+    double total_ms;
+} upr_kernel_stat;
+
+upr_status upr_profile_enable(int32_t enable);
+int32_t upr_profile_read(upr_kernel_stat* out, int32_t max_entries);
 
 /* Static description of a status code. */
 const char* upr_status_string(int32_t status);

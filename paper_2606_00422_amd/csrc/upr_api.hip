@@ -11,6 +11,7 @@
 
 #include "upr_internal.h"
 #include "upr_plan.h"
+#include "upr_profile.h"
 
 using upr::bf16;
 
@@ -117,6 +118,13 @@ upr_status check_workspace(void* ws, size_t ws_bytes, size_t need) {
             return fail(UPR_ERR_HIP, "%s failed: %s", #__VA_ARGS__, hipGetErrorString(e_));     \
     } while (0)
 
+// Launch with a named timing scope (a no-op unless profiling is enabled).
+#define UPR_LAUNCH(name, ...)                                                                   \
+    do {                                                                                        \
+        ProfScope ps_(name, s);                                                                 \
+        UPR_HIP(__VA_ARGS__);                                                                   \
+    } while (0)
+
 size_t elem_size(const upr_config& c) { return c.dtype == UPR_BF16 ? 2 : 4; }
 
 void* plane_ptr(const upr_config& c, const upr_kv_cache* cache, int layer, int kv) {
@@ -133,21 +141,30 @@ namespace upr {
 
 // Attention-output projection and FFN of one layer, on the fp32 residual g:
 // g += o Wo^T + bo;  a = LN2(g);  h = gelu(a W1^T + b1);  g += h W2^T + b2.
+// Timing scopes are named "<stage>.gemm_o" etc.
 template <typename Types>
-static hipError_t launch_ffn_block(const LayerWeights& w, const typename Types::act* o,
-                                   typename Types::act* a, typename Types::act* h, float* g,
-                                   int64_t R, int d, int F, float eps, hipStream_t s) {
+static hipError_t launch_ffn_block(const char* const names[4], const LayerWeights& w,
+                                   const typename Types::act* o, typename Types::act* a,
+                                   typename Types::act* h, float* g, int64_t R, int d, int F,
+                                   float eps, hipStream_t s) {
     using T = typename Types::kv;
     using TA = typename Types::act;
+    hipError_t e;
     Epilogue r{};
     r.mode = EPI_RESID;
     r.acc_scale = w.s_o;
     r.bias = w.bo;
     r.resid = g;
     r.ldr = d;
-    hipError_t e = launch_gemm<TA, T>(o, d, static_cast<const TA*>(w.Wo), R, d, d, r, s);
+    {
+        ProfScope ps(names[0], s);
+        e = launch_gemm<TA, T>(o, d, static_cast<const TA*>(w.Wo), R, d, d, r, s);
+    }
     if (e != hipSuccess) return e;
-    e = launch_layernorm<TA>(g, a, R, d, w.ln2_g, w.ln2_b, eps, s);
+    {
+        ProfScope ps(names[1], s);
+        e = launch_layernorm<TA>(g, a, R, d, w.ln2_g, w.ln2_b, eps, s);
+    }
     if (e != hipSuccess) return e;
     Epilogue up{};
     up.mode = EPI_GELU;
@@ -155,12 +172,21 @@ static hipError_t launch_ffn_block(const LayerWeights& w, const typename Types::
     up.bias = w.b1;
     up.out = h;
     up.ldo = F;
-    e = launch_gemm<TA, T>(a, d, static_cast<const TA*>(w.W1), R, F, d, up, s);
+    {
+        ProfScope ps(names[2], s);
+        e = launch_gemm<TA, T>(a, d, static_cast<const TA*>(w.W1), R, F, d, up, s);
+    }
     if (e != hipSuccess) return e;
     r.acc_scale = w.s_2;
     r.bias = w.b2;
+    ProfScope ps(names[3], s);
     return launch_gemm<TA, T>(h, F, static_cast<const TA*>(w.W2), R, d, F, r, s);
 }
+
+static const char* const kEncodeFfnNames[4] = {"encode.gemm_o", "encode.ln2", "encode.gemm_up",
+                                               "encode.gemm_down"};
+static const char* const kRankFfnNames[4] = {"rank.gemm_o", "rank.ln2", "rank.gemm_up",
+                                             "rank.gemm_down"};
 
 template <typename Types>
 static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_emb,
@@ -177,10 +203,10 @@ static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_
     TA* o = reinterpret_cast<TA*>(ws + p.off_o);
     TA* h = reinterpret_cast<TA*>(ws + p.off_h);
     const float qscale = 1.4426950408889634f / std::sqrt((float)D);
-    UPR_HIP(launch_resid_init<T>(hist_emb + p.row0 * d, g, R, d, s));
+    UPR_LAUNCH("encode.resid_init", launch_resid_init<T>(hist_emb + p.row0 * d, g, R, d, s));
     for (int l = 0; l < c.n_layers; ++l) {
         const LayerWeights& w = m->layers[l];
-        UPR_HIP(launch_layernorm<TA>(g, a, R, d, w.ln1_g, w.ln1_b, c.ln_eps, s));
+        UPR_LAUNCH("encode.ln1", launch_layernorm<TA>(g, a, R, d, w.ln1_g, w.ln1_b, c.ln_eps, s));
         Epilogue e{};
         e.mode = EPI_QKV_CACHE;
         e.acc_scale = w.s_qkv;
@@ -195,14 +221,15 @@ static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_
         e.row0 = p.row0;
         e.d_model = d;
         e.head_dim = D;
-        UPR_HIP(launch_gemm<TA, T>(a, d, static_cast<const TA*>(w.Wqkv), R, 3 * d, d, e, s));
+        UPR_LAUNCH("encode.gemm_qkv",
+                   launch_gemm<TA, T>(a, d, static_cast<const TA*>(w.Wqkv), R, 3 * d, d, e, s));
         if (l == c.n_layers - 1) break;     // the cache is complete; nothing reads further
-        UPR_HIP(launch_attn_encode_simple<T, TA>(q, o, R, p.row0, H, D, hist->offsets_dev,
+        UPR_LAUNCH("encode.attn", launch_attn_encode_simple<T, TA>(q, o, R, p.row0, H, D, hist->offsets_dev,
                                              hist->num_users,
                                              static_cast<const T*>(e.cache_k),
                                              static_cast<const T*>(e.cache_v),
                                              cache->capacity_rows, s));
-        UPR_HIP(launch_ffn_block<Types>(w, o, a, h, g, R, d, F, c.ln_eps, s));
+        UPR_HIP(launch_ffn_block<Types>(kEncodeFfnNames, w, o, a, h, g, R, d, F, c.ln_eps, s));
     }
     return UPR_OK;
 }
@@ -223,14 +250,14 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
     TA* o = reinterpret_cast<TA*>(ws + p.off_o);
     TA* h = reinterpret_cast<TA*>(ws + p.off_h);
     const float qscale = 1.4426950408889634f / std::sqrt((float)D);
-    UPR_HIP(launch_resid_init<T>(cand_emb + p.row0 * d, g, R, d, s));
+    UPR_LAUNCH("rank.resid_init", launch_resid_init<T>(cand_emb + p.row0 * d, g, R, d, s));
     if (p.use_mfma_attn)
-        UPR_HIP(launch_rank_worklist(cand->offsets_dev, hist->offsets_dev, cand->num_users, H,
+        UPR_LAUNCH("rank.worklist", launch_rank_worklist(cand->offsets_dev, hist->offsets_dev, cand->num_users, H,
                                      p.attn_tile, reinterpret_cast<int32_t*>(ws + p.off_work),
                                      p.work_items, s));
     for (int l = 0; l < c.n_layers; ++l) {
         const LayerWeights& w = m->layers[l];
-        UPR_HIP(launch_layernorm<TA>(g, a, R, d, w.ln1_g, w.ln1_b, c.ln_eps, s));
+        UPR_LAUNCH("rank.ln1", launch_layernorm<TA>(g, a, R, d, w.ln1_g, w.ln1_b, c.ln_eps, s));
         Epilogue e{};
         e.mode = EPI_STORE;
         e.acc_scale = w.s_qkv;
@@ -239,13 +266,14 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
         e.ldo = 3 * d;
         e.col_scale = qscale;
         e.scale_cols = d;
-        UPR_HIP(launch_gemm<TA, T>(a, d, static_cast<const TA*>(w.Wqkv), R, 3 * d, d, e, s));
+        UPR_LAUNCH("rank.gemm_qkv",
+                   launch_gemm<TA, T>(a, d, static_cast<const TA*>(w.Wqkv), R, 3 * d, d, e, s));
         const T* ck = static_cast<const T*>(plane_ptr(c, cache, l, 0));
         const T* cv = static_cast<const T*>(plane_ptr(c, cache, l, 1));
         bool done = false;
         if constexpr (std::is_same_v<Types, Bf16Types>) {
             if (p.use_mfma_attn) {
-                UPR_HIP(launch_attn_rank(qkv, o, p.row0, H, D, cand->offsets_dev,
+                UPR_LAUNCH("rank.attn", launch_attn_rank(qkv, o, p.row0, H, D, cand->offsets_dev,
                                          hist->offsets_dev,
                                          reinterpret_cast<const int32_t*>(ws + p.off_work),
                                          p.work_items, p.attn_tile, ck, cv, cache->capacity_rows,
@@ -254,12 +282,12 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
             }
         }
         if (!done)
-            UPR_HIP(launch_attn_rank_simple<T, TA>(qkv, o, R, p.row0, H, D, cand->offsets_dev,
+            UPR_LAUNCH("rank.attn", launch_attn_rank_simple<T, TA>(qkv, o, R, p.row0, H, D, cand->offsets_dev,
                                                hist->offsets_dev, cand->num_users, ck, cv,
                                                cache->capacity_rows, s));
-        UPR_HIP(launch_ffn_block<Types>(w, o, a, h, g, R, d, F, c.ln_eps, s));
+        UPR_HIP(launch_ffn_block<Types>(kRankFfnNames, w, o, a, h, g, R, d, F, c.ln_eps, s));
     }
-    UPR_HIP(launch_score_head(g, scores + p.row0, R, d, m->fin, c.ln_eps, s));
+    UPR_LAUNCH("rank.score_head", launch_score_head(g, scores + p.row0, R, d, m->fin, c.ln_eps, s));
     return UPR_OK;
 }
 

@@ -25,6 +25,7 @@ EXPORTS = (
     "upr_weights_count", "upr_model_create", "upr_model_destroy", "upr_kv_cache_bytes",
     "upr_kv_cache_index", "upr_encode_workspace_bytes", "upr_rank_workspace_bytes",
     "upr_encode_user", "upr_rank_candidates", "upr_status_string", "upr_last_error",
+    "upr_profile_enable", "upr_profile_read",
 )
 
 
@@ -41,6 +42,11 @@ class upr_segments(ctypes.Structure):
 
 class upr_kv_cache(ctypes.Structure):
     _fields_ = [("data", ctypes.c_void_p), ("capacity_rows", ctypes.c_int64)]
+
+
+class upr_kernel_stat(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("launches", ctypes.c_int64),
+                ("total_ms", ctypes.c_double)]
 
 
 class UprError(RuntimeError):
@@ -75,6 +81,8 @@ def load(path: str = LIB_PATH):
         "upr_rank_candidates": (I32, [VP, cachep, segp, VP, segp, VP, VP, SZ, VP]),
         "upr_status_string": (ctypes.c_char_p, [I32]),
         "upr_last_error": (ctypes.c_char_p, []),
+        "upr_profile_enable": (I32, [I32]),
+        "upr_profile_read": (I32, [P(upr_kernel_stat), I32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -151,6 +159,19 @@ def upr_status_string(status: int) -> str:
 
 def upr_last_error() -> str:
     return load().upr_last_error().decode()
+
+
+def upr_profile_enable(enable: bool) -> None:
+    _check(load().upr_profile_enable(1 if enable else 0))
+
+
+def upr_profile_read() -> dict:
+    """{kernel name: (launches, total_ms)} recorded since profiling was enabled."""
+    lib = load()
+    n = lib.upr_profile_read(None, 0)
+    arr = (upr_kernel_stat * max(n, 1))()
+    n = lib.upr_profile_read(arr, n)
+    return {arr[i].name.decode(): (int(arr[i].launches), float(arr[i].total_ms)) for i in range(n)}
 
 
 # ---------------------------------------------------------------------------

@@ -12,8 +12,8 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // Candidates per work item of the MFMA ranking attention (one workgroup
 // handles this many candidates of one user for one head).
-constexpr int kRankAttnTile = 128;
-constexpr bool kHaveMfmaRankAttn = false;
+constexpr int kRankAttnTile = 256;
+constexpr bool kHaveMfmaRankAttn = true;
 
 struct EncodePlan {
     int64_t row0 = 0, rows = 0;
@@ -84,6 +84,10 @@ inline RankPlan plan_rank(const upr_config& c, int U, const int32_t* coffs) {
 template <typename TA, typename TKV>
 hipError_t launch_gemm(const TA* A, int64_t lda, const TA* W, int64_t M, int N, int K,
                        const Epilogue& epi, hipStream_t s);
+
+// fp16 MFMA GEMM (K a multiple of 64, lda a multiple of 8).
+hipError_t launch_gemm_mfma(const f16* A, int64_t lda, const f16* W, int64_t M, int N, int K,
+                            const Epilogue& epi, hipStream_t s);
 
 // Work list of the MFMA ranking attention: entries (user, head, first
 // candidate row, candidate count), heaviest users first.

@@ -210,7 +210,7 @@ def main():
             b.record()
             torch.cuda.synchronize()
             lat.append(a.elapsed_time(b))
-    lat = np.array(lat)
+    lat = np.array(lat) if lat else np.array([np.nan])
 
     flops = path_flops(inp)
     out = {

@@ -27,13 +27,19 @@ FLAGS = [
 ]
 
 
+# Extra flags per source.  The attention kernel's softmax takes maxima of
+# finite logits and -inf only; without NaN semantics each max is one
+# v_max3_f32 instead of a canonicalise-then-max pair.
+FILE_FLAGS = {"k_attn_rank.hip": ["-fno-honor-nans"]}
+
+
 def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, *FILE_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

@@ -46,6 +46,30 @@ __device__ __forceinline__ int vcol(int kk) {
 
 __device__ __forceinline__ float max3(float a, float b, float c) { return fmaxf(a, fmaxf(b, c)); }
 
+// 2^x on the transcendental unit.  Softmax arguments are <= 0; results below
+// 2^-126 flush to zero, which is what a probability that small contributes.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Reductions over the four lanes {l, l^16, l^32, l^48} that hold one query:
+// v_permlane{16,32}_swap with both operands = v leaves each lane with its own
+// value and its xor-partner's, in some order.
+__device__ __forceinline__ float pair_max16(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_max32(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float quad_sum(float v) {
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+
+
 __global__ __launch_bounds__(256, 2) void k_attn_rank(
     const bf16* __restrict__ qkv, f16* __restrict__ out, int64_t row0, int H,
     const int32_t* __restrict__ hist_offsets, const int4* __restrict__ work,
@@ -84,9 +108,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
 #pragma unroll
             for (int j = 0; j < 8; ++j) s = fmaf((float)qf[qg][es][j], (float)kf[j], s);
         }
-        s += __shfl_xor(s, 16, 64);
-        s += __shfl_xor(s, 32, 64);
-        m[qg] = s;                                       // own logit
+        m[qg] = quad_sum(s);                             // own logit
         l[qg] = g == 0 ? 1.f : 0.f;                      // lane-partial sum
 #pragma unroll
         for (int eb = 0; eb < 4; ++eb) {
@@ -125,10 +147,10 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
         const uint32_t* b = reinterpret_cast<const uint32_t*>(&rv[1]);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const uint32_t lo = (j & 1) ? (a[j >> 1] >> 16) : (a[j >> 1] & 0xFFFFu);
-            const uint32_t hi = (j & 1) ? (b[j >> 1] >> 16) : (b[j >> 1] & 0xFFFFu);
+            const uint32_t pair = __builtin_amdgcn_perm(b[j >> 1], a[j >> 1],
+                                                        (j & 1) ? 0x07060302u : 0x05040100u);
             const int e = e0 + j;
-            *reinterpret_cast<uint32_t*>(&sV[buf][swz(e, col >> 3) + (col & 7)]) = lo | (hi << 16);
+            *reinterpret_cast<uint32_t*>(&sV[buf][swz(e, col >> 3) + (col & 7)]) = pair;
         }
     };
 
@@ -160,8 +182,9 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
                     s[qg][t] = acc;
                 }
             }
-            // mask keys past the history end (last sub-block only)
-            if (kbase + 32 > n) {
+            // mask keys past the history end (last sub-block only; kept off the
+            // steady-state path as an unlikely branch)
+            if (__builtin_expect(kbase + 32 > n, 0)) {
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -182,18 +205,17 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
                 mx = max3(mx, s[qg][0][3], s[qg][1][0]);
                 mx = max3(mx, s[qg][1][1], s[qg][1][2]);
                 mx = fmaxf(mx, s[qg][1][3]);
-                mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-                mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+                mx = pair_max32(pair_max16(mx));
                 const float mn = fmaxf(m[qg], mx);
                 grew |= mn > m[qg];
-                alpha[qg] = exp2f(m[qg] - mn);
+                alpha[qg] = fast_exp2(m[qg] - mn);
                 m[qg] = mn;
                 float sum = 0.f;
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
-                        const float p = exp2f(s[qg][t][r] - mn);
+                        const float p = fast_exp2(s[qg][t][r] - mn);
                         sum += p;
                         pf[qg][t * 4 + r] = (__bf16)p;
                     }
@@ -224,9 +246,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
 #pragma unroll
     for (int qg = 0; qg < 4; ++qg) {
         const int qi = wave * kQW + qg * 16 + l16;
-        float lt = l[qg];
-        lt += __shfl_xor(lt, 16, 64);
-        lt += __shfl_xor(lt, 32, 64);
+        const float lt = quad_sum(l[qg]);
         if (qi >= kc) continue;
         const float inv = 1.0f / lt;
         f16* orow = out + (c0 - row0 + qi) * (int64_t)d + h * kD;

@@ -22,6 +22,10 @@ FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
     # keep the compiler from forming packed fp32 VALU instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # no implicit multiply-add fusion: a row's arithmetic must not depend on
+    # which unrolled copy of the code handles it (candidate permutations must
+    # permute scores bit-exactly); FMAs are written out with fmaf
+    "-ffp-contract=off",
     "-Wno-unused-command-line-argument",
     "-I", INCLUDE, "-I", CSRC,
 ]

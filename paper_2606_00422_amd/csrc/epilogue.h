@@ -21,10 +21,10 @@ __device__ __forceinline__ void epilogue_apply(const Epilogue& e, int64_t m, int
     switch (e.mode) {
         case EPI_STORE:
             if (n < e.scale_cols) v *= e.col_scale;
-            static_cast<TKV*>(e.out)[m * e.ldo + n] = (TKV)v;
+            static_cast<TKV*>(e.out)[m * e.ldo + n] = (TKV)keep_f32(v);
             break;
         case EPI_GELU:
-            static_cast<TA*>(e.out)[m * e.ldo + n] = (TA)gelu_tanh_f(v);
+            static_cast<TA*>(e.out)[m * e.ldo + n] = (TA)keep_f32(gelu_tanh_f(v));
             break;
         case EPI_RESID:
             e.resid[m * e.ldr + n] += v;
@@ -32,14 +32,14 @@ __device__ __forceinline__ void epilogue_apply(const Epilogue& e, int64_t m, int
         case EPI_QKV_CACHE: {
             const int d = e.d_model;
             if (n < d) {
-                static_cast<TKV*>(e.out)[m * e.ldo + n] = (TKV)(v * e.col_scale);
+                static_cast<TKV*>(e.out)[m * e.ldo + n] = (TKV)keep_f32(v * e.col_scale);
             } else {
                 const int part = n >= 2 * d ? 2 : 1;
                 const int c = n - part * d;
                 const int h = c / e.head_dim;
                 const int ee = c - h * e.head_dim;
                 TKV* plane = static_cast<TKV*>(part == 1 ? e.cache_k : e.cache_v);
-                plane[((int64_t)h * e.cache_cap + (e.row0 + m)) * e.head_dim + ee] = (TKV)v;
+                plane[((int64_t)h * e.cache_cap + (e.row0 + m)) * e.head_dim + ee] = (TKV)keep_f32(v);
             }
             break;
         }

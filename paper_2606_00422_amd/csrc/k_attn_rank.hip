@@ -219,7 +219,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
                         sum += p;
                         pf[qg][t * 4 + r] = (__bf16)p;
                     }
-                l[qg] = l[qg] * alpha[qg] + sum;
+                l[qg] = fmaf(l[qg], alpha[qg], sum);
             }
             if (__any(grew)) {
 #pragma unroll
@@ -255,7 +255,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
             typedef __attribute__((ext_vector_type(4))) _Float16 h4;
             h4 v;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = (f16)(o[qg][eb][r] * inv);
+            for (int r = 0; r < 4; ++r) v[r] = (f16)keep_f32(o[qg][eb][r] * inv);
             *reinterpret_cast<h4*>(orow + eb * 16 + 4 * g) = v;
         }
     }

@@ -144,7 +144,7 @@ __global__ __launch_bounds__(256) void k_attn_rank_simple(
         const float v = wave_sum(acc[e] * sc);
         if (lane == e) mine = v;
     }
-    if (lane < D) o[r * d + h * D + lane] = (TA)(mine / L);
+    if (lane < D) o[r * d + h * D + lane] = (TA)keep_f32(mine / L);
 }
 
 // ---------------------------------------------------------------------------
@@ -196,7 +196,7 @@ __global__ __launch_bounds__(256) void k_attn_encode_simple(
         const float v = wave_sum(acc[e] * sc);
         if (lane == e) mine = v;
     }
-    if (lane < D) o[r * d + h * D + lane] = (TA)(mine / L);
+    if (lane < D) o[r * d + h * D + lane] = (TA)keep_f32(mine / L);
 }
 
 }  // namespace

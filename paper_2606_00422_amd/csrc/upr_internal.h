@@ -59,6 +59,16 @@ struct FinalWeights {
 
 constexpr int kMaxLayers = 64;
 
+// Materialises x as an fp32 register value.  Used right before an fp32 ->
+// fp16/bf16 conversion in code whose unrolled copies serve different rows:
+// without it the compiler may fold the producing multiply into a
+// mixed-precision instruction (one rounding) in some copies and not in others
+// (two roundings), so a row's result would depend on its position.
+__device__ __forceinline__ float keep_f32(float x) {
+    asm volatile("" : "+v"(x));
+    return x;
+}
+
 // Epilogue modes of the projection GEMMs, out = A W^T + bias, then:
 enum EpiMode : int {
     EPI_STORE = 0,      // out[m, n] (kv type); columns < scale_cols are multiplied by col_scale

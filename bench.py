@@ -53,7 +53,8 @@ def kernel_work(inp):
         "rank.ln1": ("hbm", R * d * (4.0 + es)),
         "rank.ln2": ("hbm", R * d * (4.0 + es)),
         "rank.score_head": ("hbm", R * d * 4.0 + R * 4.0),
-        "rank.resid_init": ("hbm", R * d * (es + 4.0)),
+        # read the tokens, write the fp32 residual and the normalised row
+        "rank.init_ln1": ("hbm", R * d * (es + 4.0 + es)),
     }
 
 

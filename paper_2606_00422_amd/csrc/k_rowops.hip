@@ -1,9 +1,10 @@
 // Row-wise kernels: residual-stream initialisation, LayerNorm, score head.
 //
 // One 64-lane wave owns one row of d features (d a multiple of 64, at most
-// 1024); lane j holds features j, j+64, ... so every load is a coalesced
-// 256-byte (fp32) run.  Statistics are two-pass in fp32: mean, then the mean of
-// squared deviations (population variance), as the LayerNorm definition has it.
+// 1024).  For d a multiple of 256 a lane holds float4 groups j*256 + 4*lane
+// (16-byte loads, 8-byte half stores); otherwise features lane + 64 i.
+// Statistics are two-pass in fp32 over the registers: mean, then the mean
+// of squared deviations (population variance), as LayerNorm defines them.
 #include "upr_internal.h"
 
 namespace upr {
@@ -17,38 +18,121 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 template <typename T> __device__ __forceinline__ float to_f(T v) { return (float)v; }
-template <typename T> __device__ __forceinline__ T from_f(float v) { return (T)v; }
 
 constexpr int kRowsPerBlock = 4;     // 4 waves, one row each
 constexpr int kMaxPerLane = 16;      // d <= 1024
 
-// Loads one row into registers and returns (mean, 1/sqrt(var + eps)).
-__device__ __forceinline__ void row_stats(const float* __restrict__ x, int d, int lane,
-                                          float (&v)[kMaxPerLane], float eps, float& mu,
-                                          float& rstd) {
+// Per-lane feature index of register slot i.
+template <bool VEC>
+__device__ __forceinline__ int feat(int lane, int i) {
+    return VEC ? (i >> 2) * 256 + 4 * lane + (i & 3) : lane + 64 * i;
+}
+
+template <bool VEC>
+__device__ __forceinline__ void load_row(const float* __restrict__ x, int d, int lane,
+                                         float (&v)[kMaxPerLane]) {
+    const int per = d >> 6;
+    if (VEC) {
+#pragma unroll
+        for (int j = 0; j < kMaxPerLane / 4; ++j)
+            if (4 * j < per) {
+                const float4 q = *reinterpret_cast<const float4*>(x + j * 256 + 4 * lane);
+                v[4 * j] = q.x; v[4 * j + 1] = q.y; v[4 * j + 2] = q.z; v[4 * j + 3] = q.w;
+            }
+    } else {
+#pragma unroll
+        for (int i = 0; i < kMaxPerLane; ++i)
+            if (i < per) v[i] = x[lane + 64 * i];
+    }
+}
+
+// (mean, 1/sqrt(var + eps)) of the row held in v.
+__device__ __forceinline__ void row_stats(const float (&v)[kMaxPerLane], int d, float eps,
+                                          float& mu, float& rstd) {
     const int per = d >> 6;
     float s = 0.f;
 #pragma unroll
     for (int i = 0; i < kMaxPerLane; ++i)
-        if (i < per) { v[i] = x[lane + 64 * i]; s += v[i]; }
+        if (i < per) s += v[i];
     mu = wave_sum(s) / (float)d;
     float q = 0.f;
 #pragma unroll
     for (int i = 0; i < kMaxPerLane; ++i)
-        if (i < per) { float t = v[i] - mu; q += t * t; }
+        if (i < per) { const float t = v[i] - mu; q = fmaf(t, t, q); }
     rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + eps);
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void k_resid_init(const T* __restrict__ x, float* __restrict__ g,
-                                                    int64_t n) {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (; i < n; i += stride) g[i] = to_f(x[i]);
+// Writes LN(v) (gain/shift) for the row to out (model operand type TA).
+template <bool VEC, typename TA>
+__device__ __forceinline__ void store_normed(TA* __restrict__ out, const float (&v)[kMaxPerLane],
+                                             int d, int lane, float mu, float rstd,
+                                             const float* __restrict__ gain,
+                                             const float* __restrict__ shift) {
+    const int per = d >> 6;
+    if constexpr (VEC && sizeof(TA) == 2) {
+        typedef __attribute__((ext_vector_type(4))) TA t4;
+#pragma unroll
+        for (int j = 0; j < kMaxPerLane / 4; ++j)
+            if (4 * j < per) {
+                const int c = j * 256 + 4 * lane;
+                const float4 gq = *reinterpret_cast<const float4*>(gain + c);
+                const float4 bq = *reinterpret_cast<const float4*>(shift + c);
+                t4 o;
+                o[0] = (TA)keep_f32(fmaf((v[4 * j] - mu) * rstd, gq.x, bq.x));
+                o[1] = (TA)keep_f32(fmaf((v[4 * j + 1] - mu) * rstd, gq.y, bq.y));
+                o[2] = (TA)keep_f32(fmaf((v[4 * j + 2] - mu) * rstd, gq.z, bq.z));
+                o[3] = (TA)keep_f32(fmaf((v[4 * j + 3] - mu) * rstd, gq.w, bq.w));
+                *reinterpret_cast<t4*>(out + c) = o;
+            }
+    } else {
+#pragma unroll
+        for (int i = 0; i < kMaxPerLane; ++i)
+            if (i < per) {
+                const int c = feat<VEC>(lane, i);
+                out[c] = (TA)keep_f32(fmaf((v[i] - mu) * rstd, gain[c], shift[c]));
+            }
+    }
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void k_layernorm(const float* __restrict__ g, T* __restrict__ a,
+// g = float(x); a = LN(g)  (residual stream initialisation fused with the
+// first layer's LayerNorm).
+template <bool VEC, typename TKV, typename TA>
+__global__ __launch_bounds__(256) void k_init_layernorm(const TKV* __restrict__ x,
+                                                        float* __restrict__ g, TA* __restrict__ a,
+                                                        int64_t rows, int d,
+                                                        const float* __restrict__ gain,
+                                                        const float* __restrict__ shift, float eps) {
+    const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (row >= rows) return;
+    const int per = d >> 6;
+    float v[kMaxPerLane];
+    const TKV* xr = x + row * d;
+    float* gr = g + row * d;
+#pragma unroll
+    for (int i = 0; i < kMaxPerLane; ++i)
+        if (i < per) {
+            const int c = feat<VEC>(lane, i);
+            v[i] = to_f(xr[c]);
+        }
+    if (VEC) {
+#pragma unroll
+        for (int j = 0; j < kMaxPerLane / 4; ++j)
+            if (4 * j < per)
+                *reinterpret_cast<float4*>(gr + j * 256 + 4 * lane) =
+                    make_float4(v[4 * j], v[4 * j + 1], v[4 * j + 2], v[4 * j + 3]);
+    } else {
+#pragma unroll
+        for (int i = 0; i < kMaxPerLane; ++i)
+            if (i < per) gr[lane + 64 * i] = v[i];
+    }
+    float mu, rstd;
+    row_stats(v, d, eps, mu, rstd);
+    store_normed<VEC>(a + row * d, v, d, lane, mu, rstd, gain, shift);
+}
+
+template <bool VEC, typename TA>
+__global__ __launch_bounds__(256) void k_layernorm(const float* __restrict__ g, TA* __restrict__ a,
                                                    int64_t rows, int d,
                                                    const float* __restrict__ gain,
                                                    const float* __restrict__ shift, float eps) {
@@ -56,17 +140,12 @@ __global__ __launch_bounds__(256) void k_layernorm(const float* __restrict__ g, 
     const int lane = threadIdx.x & 63;
     if (row >= rows) return;
     float v[kMaxPerLane], mu, rstd;
-    row_stats(g + row * d, d, lane, v, eps, mu, rstd);
-    T* out = a + row * d;
-    const int per = d >> 6;
-#pragma unroll
-    for (int i = 0; i < kMaxPerLane; ++i)
-        if (i < per) {
-            const int c = lane + 64 * i;
-            out[c] = from_f<T>((v[i] - mu) * rstd * gain[c] + shift[c]);
-        }
+    load_row<VEC>(g + row * d, d, lane, v);
+    row_stats(v, d, eps, mu, rstd);
+    store_normed<VEC>(a + row * d, v, d, lane, mu, rstd, gain, shift);
 }
 
+template <bool VEC>
 __global__ __launch_bounds__(256) void k_score_head(const float* __restrict__ g,
                                                     float* __restrict__ scores, int64_t rows, int d,
                                                     const float* __restrict__ gain,
@@ -77,15 +156,31 @@ __global__ __launch_bounds__(256) void k_score_head(const float* __restrict__ g,
     const int lane = threadIdx.x & 63;
     if (row >= rows) return;
     float v[kMaxPerLane], mu, rstd;
-    row_stats(g + row * d, d, lane, v, eps, mu, rstd);
+    load_row<VEC>(g + row * d, d, lane, v);
+    row_stats(v, d, eps, mu, rstd);
     const int per = d >> 6;
     float acc = 0.f;
+    if (VEC) {
 #pragma unroll
-    for (int i = 0; i < kMaxPerLane; ++i)
-        if (i < per) {
-            const int c = lane + 64 * i;
-            acc += ((v[i] - mu) * rstd * gain[c] + shift[c]) * w[c];
-        }
+        for (int j = 0; j < kMaxPerLane / 4; ++j)
+            if (4 * j < per) {
+                const int c = j * 256 + 4 * lane;
+                const float4 gq = *reinterpret_cast<const float4*>(gain + c);
+                const float4 bq = *reinterpret_cast<const float4*>(shift + c);
+                const float4 wq = *reinterpret_cast<const float4*>(w + c);
+                acc = fmaf(fmaf((v[4 * j] - mu) * rstd, gq.x, bq.x), wq.x, acc);
+                acc = fmaf(fmaf((v[4 * j + 1] - mu) * rstd, gq.y, bq.y), wq.y, acc);
+                acc = fmaf(fmaf((v[4 * j + 2] - mu) * rstd, gq.z, bq.z), wq.z, acc);
+                acc = fmaf(fmaf((v[4 * j + 3] - mu) * rstd, gq.w, bq.w), wq.w, acc);
+            }
+    } else {
+#pragma unroll
+        for (int i = 0; i < kMaxPerLane; ++i)
+            if (i < per) {
+                const int c = lane + 64 * i;
+                acc = fmaf(fmaf((v[i] - mu) * rstd, gain[c], shift[c]), w[c], acc);
+            }
+    }
     acc = wave_sum(acc);
     if (lane == 0) scores[row] = acc + b[0];
 }
@@ -96,34 +191,48 @@ inline unsigned grid_rows(int64_t rows) {
 
 }  // namespace
 
-template <typename T>
-hipError_t launch_resid_init(const T* x, float* g, int64_t rows, int d, hipStream_t s) {
-    const int64_t n = rows * d;
-    if (n == 0) return hipSuccess;
-    int64_t blocks = (n + 255) / 256;
-    if (blocks > 65536) blocks = 65536;
-    k_resid_init<T><<<(unsigned)blocks, 256, 0, s>>>(x, g, n);
+template <typename TKV, typename TA>
+hipError_t launch_init_layernorm(const TKV* x, float* g, TA* a, int64_t rows, int d,
+                                 const float* gain, const float* shift, float eps, hipStream_t s) {
+    if (rows == 0) return hipSuccess;
+    if (d % 256 == 0)
+        k_init_layernorm<true, TKV, TA><<<grid_rows(rows), 256, 0, s>>>(x, g, a, rows, d, gain,
+                                                                       shift, eps);
+    else
+        k_init_layernorm<false, TKV, TA><<<grid_rows(rows), 256, 0, s>>>(x, g, a, rows, d, gain,
+                                                                        shift, eps);
     return hipGetLastError();
 }
 
-template <typename T>
-hipError_t launch_layernorm(const float* g, T* a, int64_t rows, int d, const float* gain,
+template <typename TA>
+hipError_t launch_layernorm(const float* g, TA* a, int64_t rows, int d, const float* gain,
                             const float* shift, float eps, hipStream_t s) {
     if (rows == 0) return hipSuccess;
-    k_layernorm<T><<<grid_rows(rows), 256, 0, s>>>(g, a, rows, d, gain, shift, eps);
+    if (d % 256 == 0)
+        k_layernorm<true, TA><<<grid_rows(rows), 256, 0, s>>>(g, a, rows, d, gain, shift, eps);
+    else
+        k_layernorm<false, TA><<<grid_rows(rows), 256, 0, s>>>(g, a, rows, d, gain, shift, eps);
     return hipGetLastError();
 }
 
 hipError_t launch_score_head(const float* g, float* scores, int64_t rows, int d,
                              const FinalWeights& fw, float eps, hipStream_t s) {
     if (rows == 0) return hipSuccess;
-    k_score_head<<<grid_rows(rows), 256, 0, s>>>(g, scores, rows, d, fw.lnf_g, fw.lnf_b,
-                                                 fw.w_score, fw.b_score, eps);
+    if (d % 256 == 0)
+        k_score_head<true><<<grid_rows(rows), 256, 0, s>>>(g, scores, rows, d, fw.lnf_g, fw.lnf_b,
+                                                           fw.w_score, fw.b_score, eps);
+    else
+        k_score_head<false><<<grid_rows(rows), 256, 0, s>>>(g, scores, rows, d, fw.lnf_g,
+                                                            fw.lnf_b, fw.w_score, fw.b_score, eps);
     return hipGetLastError();
 }
 
-template hipError_t launch_resid_init<float>(const float*, float*, int64_t, int, hipStream_t);
-template hipError_t launch_resid_init<bf16>(const bf16*, float*, int64_t, int, hipStream_t);
+template hipError_t launch_init_layernorm<float, float>(const float*, float*, float*, int64_t, int,
+                                                        const float*, const float*, float,
+                                                        hipStream_t);
+template hipError_t launch_init_layernorm<bf16, f16>(const bf16*, float*, f16*, int64_t, int,
+                                                     const float*, const float*, float,
+                                                     hipStream_t);
 template hipError_t launch_layernorm<float>(const float*, float*, int64_t, int, const float*,
                                             const float*, float, hipStream_t);
 template hipError_t launch_layernorm<f16>(const float*, f16*, int64_t, int, const float*,

@@ -203,10 +203,14 @@ static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_
     TA* o = reinterpret_cast<TA*>(ws + p.off_o);
     TA* h = reinterpret_cast<TA*>(ws + p.off_h);
     const float qscale = 1.4426950408889634f / std::sqrt((float)D);
-    UPR_LAUNCH("encode.resid_init", launch_resid_init<T>(hist_emb + p.row0 * d, g, R, d, s));
+    UPR_LAUNCH("encode.init_ln1",
+               launch_init_layernorm<T, TA>(hist_emb + p.row0 * d, g, a, R, d, m->layers[0].ln1_g,
+                                            m->layers[0].ln1_b, c.ln_eps, s));
     for (int l = 0; l < c.n_layers; ++l) {
         const LayerWeights& w = m->layers[l];
-        UPR_LAUNCH("encode.ln1", launch_layernorm<TA>(g, a, R, d, w.ln1_g, w.ln1_b, c.ln_eps, s));
+        if (l > 0)
+            UPR_LAUNCH("encode.ln1",
+                       launch_layernorm<TA>(g, a, R, d, w.ln1_g, w.ln1_b, c.ln_eps, s));
         Epilogue e{};
         e.mode = EPI_QKV_CACHE;
         e.acc_scale = w.s_qkv;
@@ -250,14 +254,17 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
     TA* o = reinterpret_cast<TA*>(ws + p.off_o);
     TA* h = reinterpret_cast<TA*>(ws + p.off_h);
     const float qscale = 1.4426950408889634f / std::sqrt((float)D);
-    UPR_LAUNCH("rank.resid_init", launch_resid_init<T>(cand_emb + p.row0 * d, g, R, d, s));
+    UPR_LAUNCH("rank.init_ln1",
+               launch_init_layernorm<T, TA>(cand_emb + p.row0 * d, g, a, R, d, m->layers[0].ln1_g,
+                                            m->layers[0].ln1_b, c.ln_eps, s));
     if (p.use_mfma_attn)
         UPR_LAUNCH("rank.worklist", launch_rank_worklist(cand->offsets_dev, hist->offsets_dev, cand->num_users, H,
                                      p.attn_tile, reinterpret_cast<int32_t*>(ws + p.off_work),
                                      p.work_items, s));
     for (int l = 0; l < c.n_layers; ++l) {
         const LayerWeights& w = m->layers[l];
-        UPR_LAUNCH("rank.ln1", launch_layernorm<TA>(g, a, R, d, w.ln1_g, w.ln1_b, c.ln_eps, s));
+        if (l > 0)
+            UPR_LAUNCH("rank.ln1", launch_layernorm<TA>(g, a, R, d, w.ln1_g, w.ln1_b, c.ln_eps, s));
         Epilogue e{};
         e.mode = EPI_STORE;
         e.acc_scale = w.s_qkv;

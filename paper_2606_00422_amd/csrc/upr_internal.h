@@ -101,8 +101,10 @@ struct Epilogue {
 // Launchers (all enqueue on `stream`; they return hipGetLastError()).
 // Row-wise kernels.
 // ---------------------------------------------------------------------------
-template <typename TKV>
-hipError_t launch_resid_init(const TKV* x, float* g, int64_t rows, int d, hipStream_t s);
+// g = float(x) and a = LN(g) in one pass (first layer's LayerNorm).
+template <typename TKV, typename TA>
+hipError_t launch_init_layernorm(const TKV* x, float* g, TA* a, int64_t rows, int d,
+                                 const float* gain, const float* shift, float eps, hipStream_t s);
 template <typename TA>
 hipError_t launch_layernorm(const float* g, TA* a, int64_t rows, int d, const float* gain,
                             const float* shift, float eps, hipStream_t s);

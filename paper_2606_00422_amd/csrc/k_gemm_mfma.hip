@@ -5,16 +5,23 @@
 // Block tile 256 (rows of A) x 256 (rows of W), K in steps of 64, eight
 // waves in a 2 (M) x 4 (N) grid, each owning 128 x 64 outputs = 4 x 2 MFMA
 // tiles.  The MFMA computes the transposed tile, C^T = W A^T (W as the
-// first operand), so each lane ends up holding four CONSECUTIVE output
-// columns of one row: epilogues read/write 16 bytes (fp32 residual) or 8
-// bytes (fp16/bf16) per lane instead of scattering 2-byte values.
+// first operand), so each lane holds runs of four consecutive output
+// columns of one row.
 //
-// A and W tiles go straight from global memory into LDS (buffer loads with
-// the LDS bit: no staging registers, out-of-range rows read as zeros),
-// double-buffered: each K-step reads all its operand fragments from LDS,
-// issues the next K-step's loads, then runs its 32 MFMAs while they fly.  LDS rows are 128 bytes (64 fp16) and the
-// eight 16-byte chunks of each row are XOR-swizzled so fragment reads are
-// bank-conflict free.
+// Main loop.  A and W tiles go straight from global memory into LDS
+// (buffer loads with the LDS bit: no staging registers; rows past the end
+// read as zeros), in two stages.  LDS rows are 128 bytes (64 fp16) whose
+// eight 16-byte chunks are XOR-swizzled, so fragment reads are bank-conflict
+// free.  The two waves sharing a SIMD (w and w+4) run in opposite phases
+// ("ping-pong"): while one reads its operand fragments from LDS into
+// registers, the other runs its MFMAs, and they swap at each barrier.  Only
+// the four leading waves issue the global loads, one K-step ahead.
+//
+// Epilogue.  Stores straight from the MFMA layout touch 32 rows per
+// instruction with 8-16 bytes each and reach about 60% of the bandwidth of
+// row-contiguous stores.  Each wave therefore stages its results through its
+// own LDS region, 32 rows at a time, and writes full 128-byte (16-bit output)
+// or 256-byte (fp32 residual) row segments, 16 bytes per lane.
 //
 // Tile order is XCD-aware: workgroup b runs on XCD b % 8 and the tiles are
 // renumbered so each XCD sweeps a contiguous range of (M-panel, N-tile)
@@ -27,29 +34,23 @@ namespace upr {
 namespace gemm_detail {
 
 typedef __attribute__((ext_vector_type(8))) _Float16 h8;
-typedef __attribute__((ext_vector_type(4))) _Float16 h4;
-typedef __attribute__((ext_vector_type(4))) __bf16 b4;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
 
-// Tile shapes.  Big: 256x256, K-step 64, 8 waves of 128x64, one workgroup
-// per CU (128 KB LDS).  Wide: 256x128, K-step 32, 4 waves of 128x64, two
-// workgroups per CU (48 KB LDS each), so one workgroup's epilogue overlaps
-// the other's MFMAs.
-template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int MIN_BLOCKS_>
-struct Tile {
-    static constexpr int BM = BM_, BN = BN_, BK = BK_;
-    static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_;
-    static constexpr int THREADS = 64 * WAVES_M * WAVES_N, MIN_BLOCKS = MIN_BLOCKS_;
-    static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;     // per-wave tile
-    static constexpr int TM = WM / 32, TN = WN / 32;               // 32x32 MFMA tiles
-    static constexpr int CPR = BK / 8;                             // 16-byte chunks per LDS row
-    static constexpr int RPB = 16 / CPR;                           // rows per 256-byte bank line
-    static constexpr int LOADS_A = BM * CPR / THREADS, LOADS_B = BN * CPR / THREADS;
-    static_assert(BM * CPR % (THREADS) == 0 && BN * CPR % THREADS == 0, "whole loads per thread");
-    static_assert(LOADS_A % 1 == 0 && 64 % CPR == 0, "a wave's load covers whole rows");
-};
-using TileBig = Tile<256, 256, 64, 2, 4, 1>;
-using TileWide = Tile<256, 128, 32, 2, 2, 2>;
+constexpr int kBM = 256, kBN = 256, kBK = 64;     // block tile
+constexpr int kThreads = 512;                      // 8 waves
+constexpr int kWavesN = 4;
+constexpr int kWM = 128, kWN = 64;                 // per-wave tile
+constexpr int kTM = kWM / 32, kTN = kWN / 32;      // 32x32 MFMA tiles per wave
+constexpr int kCPR = kBK / 8;                      // 16-byte chunks per LDS row (8)
+constexpr int kLoadsA = 2 * kBM * kCPR / kThreads; // per leading wave per K-step (8)
+constexpr int kLoadsB = 2 * kBN * kCPR / kThreads;
+// Epilogue staging row strides (elements).  16-bit: 144 bytes, so the 16
+// rows written by one 16-lane group of 16-byte stores fall on distinct bank
+// groups and rows 8 apart on disjoint halves; fp32: 272 bytes, likewise for
+// the 16-byte fp32 writes.
+constexpr int kStage16 = 72, kStage32 = 68;
+constexpr int kRegionBytes = 16384;                // LDS staging region per wave
 
 __device__ __forceinline__ int xcd_tile(int b, int nb) {
     const int per = nb >> 3, rem = nb & 7;
@@ -58,13 +59,12 @@ __device__ __forceinline__ int xcd_tile(int b, int nb) {
 }
 
 // gfx950's LDS serves a 16-byte access for 16 lanes per pass across 64 banks
-// (256 bytes = RPB rows).  Fragment reads take 16 consecutive rows at one
-// logical chunk; rows with equal (row % RPB) share bank slots, so the chunk
-// is XORed with (row / RPB) % CPR to spread them.  Element offset of logical
-// chunk `chunk` of row `row`:
-template <class TL>
+// (256 bytes = 2 rows).  Fragment reads take 16 consecutive rows at one
+// logical chunk; the chunk is XORed with (row / 2) % 8 so those rows land
+// on distinct bank groups.  Element offset of logical chunk `chunk` of row
+// `row`:
 __device__ __forceinline__ int swz(int row, int chunk) {
-    return row * TL::BK + ((chunk ^ ((row / TL::RPB) % TL::CPR)) << 3);
+    return row * kBK + ((chunk ^ ((row >> 1) & 7)) << 3);
 }
 
 // GELU, tanh form, as x * sigmoid(2y) with y = sqrt(2/pi) (x + 0.044715 x^3):
@@ -76,15 +76,30 @@ __device__ __forceinline__ float gelu_fast(float x) {
     return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z));
 }
 
-template <class TL, int MODE, typename TKV>
-__device__ __forceinline__ void gemm_tile(const f16* __restrict__ A, int64_t lda,
-                                          const f16* __restrict__ W, int64_t M, int N, int K,
-                                          const Epilogue& epi) {
-    constexpr int kBM = TL::BM, kBN = TL::BN, kBK = TL::BK;
-    constexpr int kWavesN = TL::WAVES_N, kWM = TL::WM, kWN = TL::WN, kTM = TL::TM, kTN = TL::TN;
-    constexpr int kCPR = TL::CPR;
-    __shared__ __attribute__((aligned(16))) f16 sA[2][kBM * kBK];
-    __shared__ __attribute__((aligned(16))) f16 sB[2][kBN * kBK];
+// Two values rounded to bf16 (BF) or fp16, packed low-first.
+template <bool BF>
+__device__ __forceinline__ unsigned pack2(float a, float b) {
+    unsigned short x, y;
+    if constexpr (BF) {
+        x = __builtin_bit_cast(unsigned short, (__bf16)keep_f32(a));
+        y = __builtin_bit_cast(unsigned short, (__bf16)keep_f32(b));
+    } else {
+        x = __builtin_bit_cast(unsigned short, (_Float16)keep_f32(a));
+        y = __builtin_bit_cast(unsigned short, (_Float16)keep_f32(b));
+    }
+    return (unsigned)x | ((unsigned)y << 16);
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict__ A, int64_t lda,
+                                                           const f16* __restrict__ W, int64_t M,
+                                                           int N, int K, Epilogue epi) {
+    // Two LDS stages as separate arrays: the compiler can then tell that
+    // fragment reads of one stage do not alias the loads filling the other.
+    __shared__ __attribute__((aligned(16))) f16 sA0[kBM * kBK];
+    __shared__ __attribute__((aligned(16))) f16 sA1[kBM * kBK];
+    __shared__ __attribute__((aligned(16))) f16 sB0[kBN * kBK];
+    __shared__ __attribute__((aligned(16))) f16 sB1[kBN * kBK];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / kWavesN, wn = wave % kWavesN;
@@ -92,6 +107,7 @@ __device__ __forceinline__ void gemm_tile(const f16* __restrict__ A, int64_t lda
     const int t = xcd_tile(blockIdx.x, gridDim.x);
     const int64_t m0 = (int64_t)(t / tiles_n) * kBM;
     const int n0 = (t % tiles_n) * kBN;
+    const bool lead = __builtin_amdgcn_readfirstlane(wave) < 4;
 
     // Buffer descriptors over this tile's rows of A and W: rows past M (N)
     // fall outside num_records and load as zeros, so tails need no branches.
@@ -102,35 +118,38 @@ __device__ __forceinline__ void gemm_tile(const f16* __restrict__ A, int64_t lda
     const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(W + (int64_t)n0 * K), (short)0, (int)((int64_t)rows_b * K * 2), 0x00020000);
 
-    // Direct global -> LDS loads: a wave's 64 lanes fill 64 consecutive
-    // 16-byte LDS slots.  Slot s of row r must hold logical chunk
-    // s ^ key(r), so that is the chunk each lane fetches.
-    int offA[TL::LOADS_A], offB[TL::LOADS_B];
+    // Direct global -> LDS loads by the leading waves: a load instruction's
+    // 64 lanes fill 64 consecutive 16-byte LDS slots = 8 rows.  Load i of
+    // leading wave lw covers rows 8 (lw kL + i) + lane/8; slot s of row r
+    // must hold logical chunk s ^ key(r), key(r) = (r / 2) % 8, which
+    // depends on i only through i % 2.  So two per-lane offsets plus a
+    // uniform step of 16 rows address every load.  (The step stays in the
+    // per-lane offset: the buffer range check that zero-fills rows past the
+    // end does not cover the scalar offset.)
+    const int lw = wave & 3;
+    int voA[2], voB[2];
 #pragma unroll
-    for (int i = 0; i < TL::LOADS_A; ++i) {
-        const int c = (wave * TL::LOADS_A + i) * 64 + lane;
-        const int row = c / kCPR, slot = c % kCPR;
-        const int lch = slot ^ ((row / TL::RPB) % kCPR);
-        offA[i] = (int)(row * lda * 2 + lch * 16);
+    for (int p = 0; p < 2; ++p) {
+        const int lch = (lane & 7) ^ ((p * 4 + (lane >> 4)) & 7);
+        voA[p] = (int)(((lw * kLoadsA + p) * 8 + (lane >> 3)) * lda * 2 + lch * 16);
+        voB[p] = ((lw * kLoadsB + p) * 8 + (lane >> 3)) * K * 2 + lch * 16;
     }
+    const int rowstepA = (int)(16 * lda * 2), rowstepB = 16 * K * 2;
+    auto issue_loads = [&](f16* dA, f16* dB, int k0) {
+        // opaque copies keep the per-load offsets from being hoisted into
+        // sixteen live registers
+        int rsa = rowstepA, rsb = rowstepB;
+        asm volatile("" : "+s"(rsa), "+s"(rsb));
 #pragma unroll
-    for (int i = 0; i < TL::LOADS_B; ++i) {
-        const int c = (wave * TL::LOADS_B + i) * 64 + lane;
-        const int row = c / kCPR, slot = c % kCPR;
-        const int lch = slot ^ ((row / TL::RPB) % kCPR);
-        offB[i] = row * K * 2 + lch * 16;
-    }
-    auto issue_loads = [&](int buf, int k0) {
-#pragma unroll
-        for (int i = 0; i < TL::LOADS_A; ++i)
+        for (int i = 0; i < kLoadsA; ++i)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rsA, (__attribute__((address_space(3))) void*)(&sA[buf][(wave * TL::LOADS_A + i) * 64 * 8]),
-                16, offA[i] + k0 * 2, 0, 0, 0);
+                rsA, (__attribute__((address_space(3))) void*)(dA + (lw * kLoadsA + i) * 64 * 8),
+                16, voA[i & 1] + (i >> 1) * rsa + k0 * 2, 0, 0, 0);
 #pragma unroll
-        for (int i = 0; i < TL::LOADS_B; ++i)
+        for (int i = 0; i < kLoadsB; ++i)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rsB, (__attribute__((address_space(3))) void*)(&sB[buf][(wave * TL::LOADS_B + i) * 64 * 8]),
-                16, offB[i] + k0 * 2, 0, 0, 0);
+                rsB, (__attribute__((address_space(3))) void*)(dB + (lw * kLoadsB + i) * 64 * 8),
+                16, voB[i & 1] + (i >> 1) * rsb + k0 * 2, 0, 0, 0);
     };
 
     f32x16 acc[kTN][kTM];
@@ -142,26 +161,20 @@ __device__ __forceinline__ void gemm_tile(const f16* __restrict__ A, int64_t lda
             for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
 
     const int lrow = lane & 31, lhalf = lane >> 5;
-    // One K-step: read all of its operand fragments from LDS buffer `buf`
-    // first, then issue the next K-step's loads, then run the MFMAs.  The
-    // order matters: the compiler waits for outstanding LDS-DMA loads before
-    // any later LDS read (it cannot see that they target the other buffer),
-    // so reads issued after the DMA would serialise load and compute.
-    auto step = [&](int buf, int next_k0, bool issue_next) {
-        h8 a[kBK / 16][kTM], b[kBK / 16][kTN];
+    h8 a[kBK / 16][kTM], b[kBK / 16][kTN];
+    auto read_frags = [&](const f16* cA, const f16* cB) {
 #pragma unroll
         for (int kk = 0; kk < kBK / 16; ++kk) {
             const int ch = kk * 2 + lhalf;
 #pragma unroll
             for (int i = 0; i < kTM; ++i)
-                a[kk][i] = *reinterpret_cast<const h8*>(&sA[buf][swz<TL>(wm * kWM + i * 32 + lrow, ch)]);
+                a[kk][i] = *reinterpret_cast<const h8*>(&cA[swz(wm * kWM + i * 32 + lrow, ch)]);
 #pragma unroll
             for (int j = 0; j < kTN; ++j)
-                b[kk][j] = *reinterpret_cast<const h8*>(&sB[buf][swz<TL>(wn * kWN + j * 32 + lrow, ch)]);
+                b[kk][j] = *reinterpret_cast<const h8*>(&cB[swz(wn * kWN + j * 32 + lrow, ch)]);
         }
-        __builtin_amdgcn_sched_barrier(0);
-        if (issue_next) issue_loads(buf ^ 1, next_k0);
-        __builtin_amdgcn_sched_barrier(0);
+    };
+    auto compute = [&]() {
 #pragma unroll
         for (int kk = 0; kk < kBK / 16; ++kk)
 #pragma unroll
@@ -170,157 +183,218 @@ __device__ __forceinline__ void gemm_tile(const f16* __restrict__ A, int64_t lda
                 for (int i = 0; i < kTM; ++i)
                     acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(b[kk][j], a[kk][i],
                                                                        acc[j][i], 0, 0, 0);
-        // keep the end-of-step wait and barrier behind the MFMAs
+    };
+
+    // Every wave runs the same read / MFMA sequence; the trailing waves run
+    // it one phase late (one extra barrier at the start, the leading waves
+    // one at the end).  K-step t sits in stage t & 1.  The leading waves
+    // issue step t+1's loads at the start of their step t into the other
+    // stage (last read by the trailing waves in the phase just ended) and
+    // wait for them at the end of step t, before anyone reads them.
+    const int nk = K / kBK;
+    auto kstep = [&](const f16* cA, const f16* cB, f16* nA, f16* nB, int t) {
+        if (lead && t + 1 < nk) issue_loads(nA, nB, (t + 1) * kBK);
+        read_frags(cA, cB);
+        __builtin_amdgcn_s_waitcnt(0xC07F);     // lgkmcnt(0): fragments in registers
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        compute();
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(0x0F70);     // vmcnt(0): the next stage has landed
+        __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_sched_barrier(0);
     };
 
-    // K-step j lives in LDS buffer j&1.  Step kt computes from buffer kt&1
-    // while the loads of kt+1 fill the other buffer (free: its last readers
-    // passed the previous barrier); each wave waits for its own loads before
-    // the barrier that publishes the buffer.
-    const int nk = K / kBK;
-    issue_loads(0, 0);
+    if (lead) issue_loads(sA0, sB0, 0);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        step(kt & 1, (kt + 1) * kBK, kt + 1 < nk);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
+    if (!lead) __builtin_amdgcn_s_barrier();
+    int kt = 0;
+    for (; kt + 2 <= nk; kt += 2) {
+        kstep(sA0, sB0, sA1, sB1, kt);
+        kstep(sA1, sB1, sA0, sB0, kt + 1);
     }
+    if (kt < nk) kstep(sA0, sB0, sA1, sB1, kt);
+    // Past here every wave has finished its fragment reads (the trailing
+    // waves' last reads precede the barrier that ended the leading waves'
+    // last step), so the stages are free for the epilogue; the leading
+    // waves' epilogue overlaps the trailing waves' last MFMAs.
 
-    // Epilogue.  Register r of transposed tile (j, i) holds output row
-    // m0 + wm*128 + 32i + lane%32 and column n0 + wn*64 + 32j + 8(r/4) + 4(lane/32) + r%4.
-    // All loads are issued before their uses (bias once per tile, the fp32
-    // residual once per row-tile) so their latencies overlap.
-    const float* __restrict__ bias_p = epi.bias;
+    // ---- epilogue ------------------------------------------------------
+    // Register r of transposed tile (j, i) holds output row
+    // wm*128 + 32i + lane%32 and column wn*64 + 32j + 8(r/4) + 4(lane/32) + r%4.
+    const int wsel = __builtin_amdgcn_readfirstlane(wave) >> 1;
+    f16* const sbase = wsel == 0 ? sA0 : wsel == 1 ? sA1 : wsel == 2 ? sB0 : sB1;
+    char* const region = reinterpret_cast<char*>(sbase) + (wave & 1) * kRegionBytes;
+    const int64_t wrow0 = m0 + wm * kWM;
+    const int wcol0 = n0 + wn * kWN;
     float4 bq[kTN][4];
 #pragma unroll
     for (int j = 0; j < kTN; ++j)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const int col = n0 + wn * kWN + j * 32 + 8 * q + 4 * lhalf;
-            bq[j][q] = col < N ? *reinterpret_cast<const float4*>(bias_p + col)
+            const int col = wcol0 + j * 32 + 8 * q + 4 * lhalf;
+            bq[j][q] = col < N ? *reinterpret_cast<const float4*>(epi.bias + col)
                                : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     const float sc = epi.acc_scale;
+
+    if constexpr (MODE == EPI_RESID) {
+        // fp32 staging: a lane writes its four-column runs (16 bytes); reads
+        // give 16 lanes per 256-byte row segment, 4 rows per instruction.
+        float* const st = reinterpret_cast<float*>(region);
+        const int ch = lane & 15;
+        const int col = wcol0 + ch * 4;
 #pragma unroll
-    for (int i = 0; i < kTM; ++i) {
-        const int64_t row = m0 + wm * kWM + i * 32 + lrow;
-        if (row >= M) continue;
-        float4 v[kTN][4];
+        for (int i = 0; i < kTM; ++i) {
 #pragma unroll
-        for (int j = 0; j < kTN; ++j)
+            for (int j = 0; j < kTN; ++j)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                v[j][q].x = fmaf(acc[j][i][4 * q + 0], sc, bq[j][q].x);
-                v[j][q].y = fmaf(acc[j][i][4 * q + 1], sc, bq[j][q].y);
-                v[j][q].z = fmaf(acc[j][i][4 * q + 2], sc, bq[j][q].z);
-                v[j][q].w = fmaf(acc[j][i][4 * q + 3], sc, bq[j][q].w);
+                for (int q = 0; q < 4; ++q) {
+                    float4 v;
+                    v.x = fmaf(acc[j][i][4 * q + 0], sc, bq[j][q].x);
+                    v.y = fmaf(acc[j][i][4 * q + 1], sc, bq[j][q].y);
+                    v.z = fmaf(acc[j][i][4 * q + 2], sc, bq[j][q].z);
+                    v.w = fmaf(acc[j][i][4 * q + 3], sc, bq[j][q].w);
+                    *reinterpret_cast<float4*>(st + lrow * kStage32 + j * 32 + 8 * q + 4 * lhalf) = v;
+                }
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            __builtin_amdgcn_wave_barrier();
+            float4 x[8], g[8];
+#pragma unroll
+            for (int p = 0; p < 8; ++p) {
+                const int rl = p * 4 + (lane >> 4);
+                const int64_t row = wrow0 + i * 32 + rl;
+                x[p] = *reinterpret_cast<const float4*>(st + rl * kStage32 + ch * 4);
+                if (row < M && col < N)
+                    g[p] = *reinterpret_cast<const float4*>(epi.resid + row * epi.ldr + col);
             }
-        if constexpr (MODE == EPI_RESID) {
-            float* __restrict__ rrow = epi.resid + row * epi.ldr;
-            float4 g[kTN][4];
 #pragma unroll
-            for (int j = 0; j < kTN; ++j)
+            for (int p = 0; p < 8; ++p) {
+                const int64_t row = wrow0 + i * 32 + p * 4 + (lane >> 4);
+                if (row >= M || col >= N) continue;
+                float4 o = g[p];
+                o.x += x[p].x; o.y += x[p].y; o.z += x[p].z; o.w += x[p].w;
+                *reinterpret_cast<float4*>(epi.resid + row * epi.ldr + col) = o;
+            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            __builtin_amdgcn_wave_barrier();
+        }
+    } else {
+        // 16-bit staging.  After conversion, lane pairs (l, l+32) exchange
+        // halves with v_permlane32_swap so each lane holds eight consecutive
+        // columns (16 bytes): lane l gets columns 16c + 8(l/32) + 0..7, c = 0, 1,
+        // of each 32-column tile.  Reads give 8 lanes per 128-byte row
+        // segment; the two rows of a 16-lane group are 8 apart (bank-disjoint).
+        constexpr bool kBf = MODE != EPI_GELU;
+        unsigned short* const st = reinterpret_cast<unsigned short*>(region);
+        const int ch = lane & 7, rs = lane >> 3;
+        const int col = wcol0 + ch * 8;
+#pragma unroll
+        for (int i = 0; i < kTM; ++i) {
+#pragma unroll
+            for (int j = 0; j < kTN; ++j) {
+                unsigned pk[4][2];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int col = n0 + wn * kWN + j * 32 + 8 * q + 4 * lhalf;
-                    if (col < N) g[j][q] = *reinterpret_cast<const float4*>(rrow + col);
-                }
-#pragma unroll
-            for (int j = 0; j < kTN; ++j)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int col = n0 + wn * kWN + j * 32 + 8 * q + 4 * lhalf;
-                    if (col >= N) continue;
-                    float4 o = g[j][q];
-                    o.x += v[j][q].x; o.y += v[j][q].y; o.z += v[j][q].z; o.w += v[j][q].w;
-                    *reinterpret_cast<float4*>(rrow + col) = o;
-                }
-        } else {
-#pragma unroll
-            for (int j = 0; j < kTN; ++j)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int col = n0 + wn * kWN + j * 32 + 8 * q + 4 * lhalf;
-                    if (col >= N) continue;          // N is a multiple of 4
-                    const float vv[4] = {v[j][q].x, v[j][q].y, v[j][q].z, v[j][q].w};
+                    float v[4];
+                    v[0] = fmaf(acc[j][i][4 * q + 0], sc, bq[j][q].x);
+                    v[1] = fmaf(acc[j][i][4 * q + 1], sc, bq[j][q].y);
+                    v[2] = fmaf(acc[j][i][4 * q + 2], sc, bq[j][q].z);
+                    v[3] = fmaf(acc[j][i][4 * q + 3], sc, bq[j][q].w);
                     if constexpr (MODE == EPI_GELU) {
-                        h4 o;
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) o[r] = (f16)keep_f32(gelu_fast(vv[r]));
-                        *reinterpret_cast<h4*>(static_cast<f16*>(epi.out) + row * epi.ldo + col) = o;
-                    } else if constexpr (MODE == EPI_STORE) {
-                        const float cs = col < epi.scale_cols ? epi.col_scale : 1.0f;
-                        b4 o;
+                        for (int r = 0; r < 4; ++r) v[r] = gelu_fast(v[r]);
+                    } else {
+                        // EPI_STORE: columns < scale_cols scaled; EPI_QKV_CACHE:
+                        // the query columns (< d_model) scaled
+                        const int c4 = wcol0 + j * 32 + 8 * q + 4 * lhalf;
+                        const int lim = MODE == EPI_STORE ? epi.scale_cols : epi.d_model;
+                        const float cs = c4 < lim ? epi.col_scale : 1.0f;
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) o[r] = (__bf16)keep_f32(vv[r] * cs);
-                        *reinterpret_cast<b4*>(static_cast<bf16*>(epi.out) + row * epi.ldo + col) = o;
-                    } else {   // EPI_QKV_CACHE: 4 columns never straddle a head (head_dim % 4 == 0)
-                        const int d = epi.d_model;
-                        b4 o;
-                        bf16* dst;
-                        if (col < d) {
-#pragma unroll
-                            for (int r = 0; r < 4; ++r) o[r] = (__bf16)keep_f32(vv[r] * epi.col_scale);
-                            dst = static_cast<bf16*>(epi.out) + row * epi.ldo + col;
-                        } else {
-                            const int part = col >= 2 * d ? 2 : 1;
-                            const int c = col - part * d;
-                            const int h = c / epi.head_dim, e = c - h * epi.head_dim;
-#pragma unroll
-                            for (int r = 0; r < 4; ++r) o[r] = (__bf16)keep_f32(vv[r]);
-                            bf16* plane = static_cast<bf16*>(part == 1 ? epi.cache_k : epi.cache_v);
-                            dst = plane + ((int64_t)h * epi.cache_cap + (epi.row0 + row)) * epi.head_dim + e;
-                        }
-                        *reinterpret_cast<b4*>(dst) = o;
+                        for (int r = 0; r < 4; ++r) v[r] = v[r] * cs;
                     }
+                    pk[q][0] = pack2<kBf>(v[0], v[1]);
+                    pk[q][1] = pack2<kBf>(v[2], v[3]);
                 }
+#pragma unroll
+                for (int c = 0; c < 2; ++c) {
+                    u32x4 o;
+#pragma unroll
+                    for (int w = 0; w < 2; ++w) {
+                        const auto r = __builtin_amdgcn_permlane32_swap(pk[2 * c][w], pk[2 * c + 1][w],
+                                                                        false, false);
+                        o[w] = r[0];
+                        o[2 + w] = r[1];
+                    }
+                    *reinterpret_cast<u32x4*>(st + lrow * kStage16 + j * 32 + 16 * c + 8 * lhalf) = o;
+                }
+            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                const int rl = 16 * (p >> 1) + 4 * (p & 1) + (rs >> 1) + 8 * (rs & 1);
+                const u32x4 o = *reinterpret_cast<const u32x4*>(st + rl * kStage16 + ch * 8);
+                const int64_t row = wrow0 + i * 32 + rl;
+                if (row >= M || col >= N) continue;          // N is a multiple of 8
+                unsigned short* dst;
+                if constexpr (MODE == EPI_QKV_CACHE) {
+                    const int d = epi.d_model;
+                    if (col < d) {
+                        dst = static_cast<unsigned short*>(epi.out) + row * epi.ldo + col;
+                    } else {   // 8 columns never straddle a head (head_dim % 8 == 0)
+                        const int part = col >= 2 * d ? 2 : 1;
+                        const int c = col - part * d;
+                        const int h = c / epi.head_dim, e = c - h * epi.head_dim;
+                        unsigned short* plane =
+                            static_cast<unsigned short*>(part == 1 ? epi.cache_k : epi.cache_v);
+                        dst = plane + ((int64_t)h * epi.cache_cap + (epi.row0 + row)) * epi.head_dim + e;
+                    }
+                } else {
+                    dst = static_cast<unsigned short*>(epi.out) + row * epi.ldo + col;
+                }
+                *reinterpret_cast<u32x4*>(dst) = o;
+            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            __builtin_amdgcn_wave_barrier();
         }
     }
+    if (lead) __builtin_amdgcn_s_barrier();
 }
 
-template <class TL, int MODE, typename TKV>
-__global__ __launch_bounds__(TL::THREADS, TL::MIN_BLOCKS) void k_gemm_mfma(
-    const f16* __restrict__ A, int64_t lda, const f16* __restrict__ W, int64_t M, int N, int K,
-    Epilogue epi) {
-    gemm_tile<TL, MODE, TKV>(A, lda, W, M, N, K, epi);
-}
-
-template <class TL, int MODE>
+template <int MODE>
 hipError_t launch_mode(const f16* A, int64_t lda, const f16* W, int64_t M, int N, int K,
                        const Epilogue& epi, hipStream_t s) {
-    const int64_t tiles = ((M + TL::BM - 1) / TL::BM) * (int64_t)((N + TL::BN - 1) / TL::BN);
-    k_gemm_mfma<TL, MODE, bf16><<<(unsigned)tiles, TL::THREADS, 0, s>>>(A, lda, W, M, N, K, epi);
+    const int64_t tiles = ((M + kBM - 1) / kBM) * (int64_t)((N + kBN - 1) / kBN);
+    k_gemm_mfma<MODE><<<(unsigned)tiles, kThreads, 0, s>>>(A, lda, W, M, N, K, epi);
     return hipGetLastError();
-}
-
-template <class TL>
-hipError_t launch_tile(const f16* A, int64_t lda, const f16* W, int64_t M, int N, int K,
-                       const Epilogue& epi, hipStream_t s) {
-    switch (epi.mode) {
-        case EPI_STORE: return launch_mode<TL, EPI_STORE>(A, lda, W, M, N, K, epi, s);
-        case EPI_GELU: return launch_mode<TL, EPI_GELU>(A, lda, W, M, N, K, epi, s);
-        case EPI_RESID: return launch_mode<TL, EPI_RESID>(A, lda, W, M, N, K, epi, s);
-        case EPI_QKV_CACHE: return launch_mode<TL, EPI_QKV_CACHE>(A, lda, W, M, N, K, epi, s);
-        default: return hipErrorInvalidValue;
-    }
 }
 
 }  // namespace gemm_detail
 
-using gemm_detail::TileBig;
-using gemm_detail::TileWide;
-using gemm_detail::launch_tile;
-
-#ifndef GEMM_TILE_CHOICE
-#define GEMM_TILE_CHOICE launch_tile<TileBig>
-#endif
 hipError_t launch_gemm_mfma(const f16* A, int64_t lda, const f16* W, int64_t M, int N, int K,
                             const Epilogue& epi, hipStream_t s) {
+    using namespace gemm_detail;
     if (M == 0) return hipSuccess;
-    if (K % 64 != 0 || lda % 8 != 0 || N % 4 != 0) return hipErrorInvalidValue;
-    return GEMM_TILE_CHOICE(A, lda, W, M, N, K, epi, s);
+    // whole 64-deep K-steps, 16-byte operand loads, 16-byte output chunks
+    if (K <= 0 || K % kBK != 0 || lda % 8 != 0 || N % 8 != 0) return hipErrorInvalidValue;
+    switch (epi.mode) {
+        case EPI_STORE:
+            if (epi.ldo % 8 != 0 || epi.scale_cols % 4 != 0) return hipErrorInvalidValue;
+            return launch_mode<EPI_STORE>(A, lda, W, M, N, K, epi, s);
+        case EPI_GELU:
+            if (epi.ldo % 8 != 0) return hipErrorInvalidValue;
+            return launch_mode<EPI_GELU>(A, lda, W, M, N, K, epi, s);
+        case EPI_RESID:
+            if (epi.ldr % 4 != 0) return hipErrorInvalidValue;
+            return launch_mode<EPI_RESID>(A, lda, W, M, N, K, epi, s);
+        case EPI_QKV_CACHE:
+            if (epi.ldo % 8 != 0 || epi.head_dim % 8 != 0 || epi.d_model % 8 != 0)
+                return hipErrorInvalidValue;
+            return launch_mode<EPI_QKV_CACHE>(A, lda, W, M, N, K, epi, s);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace upr

@@ -7,47 +7,65 @@
 //
 // One workgroup = one work item (user, head, up to 256 candidates); four
 // waves of 64 candidates.  The user's cached K/V for this layer and head are
-// streamed through LDS in 64-key stages (double-buffered) and shared by all
-// 256 candidates of the item.  Per 32-key sub-block each wave computes
+// streamed through LDS in 64-key stages (double-buffered, loaded straight
+// from global memory into LDS) and shared by all 256 candidates of the item.
+// Per 32-key sub-block each wave computes
 //   S^T = K Q^T        (v_mfma_f32_16x16x32_bf16, keys x queries),
 // so a lane holds 8 logits of ONE query (keys 4g..4g+3 and 16+4g..16+4g+3,
-// g = lane/16); the running max / sum of a query need only 2 cross-lane
-// steps.  The probabilities, packed to bf16, are directly the B operand of
-//   O^T += V^T P^T     (e x queries),
-// provided V^T's columns in LDS follow the same key order, which the staging
-// transpose writes.  The online softmax starts from the candidate's own
-// logit and value (m = s_self, l = 1, O = v_self), then folds in history.
+// g = lane/16).  The probabilities, packed to bf16, are directly the B
+// operand of
+//   O^T += V^T P^T     (e x queries);
+// V stays row-major in LDS and the transposing LDS read (ds_read_b64_tr_b16)
+// delivers V^T fragments in that same key order.
+//
+// Softmax against a fixed reference: each query's reference logit m is its
+// own logit (p_self = 1, l = 1, O = v_self to start).  The logit MFMA
+// accumulates onto -m, giving s - m directly, and p = 2^(s - m) with no
+// running maximum and no rescaling of O: probabilities up to 2^kTau are
+// accumulated as they are (fp32 sums, bf16 probabilities: relative precision
+// does not depend on magnitude), and the normaliser uses the same reference.
+// A work item in which some logit exceeds its reference by more than kTau
+// (a logit range no LayerNorm'd model produces) is redone exactly: a first
+// pass finds each query's maximum logit, and the second runs against it.
+// Row sums use v_dot2 over the bf16 probabilities, the same values that
+// weight V.
 #include "upr_plan.h"
+
+#include <cstdlib>
 
 namespace upr {
 
 namespace {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 b8;
+typedef __attribute__((ext_vector_type(2))) __bf16 b2;
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 b4v;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 
 constexpr int kD = 64;            // head_dim
 constexpr int kQW = 64;           // queries per wave
 constexpr int kTQ = 4 * kQW;      // queries per work item
 constexpr int kKS = 64;           // keys per LDS stage
+constexpr float kTau = 64.0f;     // log2 headroom above the softmax reference (maximum)
 static_assert(kTQ == kRankAttnTile, "work-list tile must match the kernel");
 
-// LDS element offset of 16-byte chunk `ch` of 128-byte row `row`, XOR-swizzled.
-__device__ __forceinline__ int swz(int row, int ch) { return row * 64 + ((ch ^ (row & 7)) << 3); }
-
-// Column of key kk (0..63 inside a stage) in the transposed V tile: key order
-// of the PV B-operand (k-index 8g+j <-> key 4g+j for j<4, 16+4g+(j-4) for j>=4,
-// within each 32-key half).
-__device__ __forceinline__ int vcol(int kk) {
-    const int half = kk >> 5, k = kk & 31;
-    const int hi = k >> 4, kr = k & 15;
-    return half * 32 + ((kr >> 2) << 3) + (hi << 2) + (kr & 3);
-}
+// LDS layout of a stage: 64 rows (keys) x 128 bytes (64 dims), the eight
+// 16-byte chunks of a row XOR-swizzled.  K fragment reads take 16
+// consecutive rows at one chunk: key (row / 2) % 8 puts them on distinct bank
+// groups.  V transposing reads take 8 consecutive rows x 32 bytes per
+// 32-lane pass: key 2 ((row / 2) % 4) keeps the two chunks of a 32-byte pair
+// together and puts equal-parity rows on distinct pairs.
+__device__ __forceinline__ int key_k(int row) { return (row >> 1) & 7; }
+__device__ __forceinline__ int key_v(int row) { return ((row >> 1) & 3) << 1; }
 
 __device__ __forceinline__ float max3(float a, float b, float c) { return fmaxf(a, fmaxf(b, c)); }
 
-// 2^x on the transcendental unit.  Softmax arguments are <= 0; results below
-// 2^-126 flush to zero, which is what a probability that small contributes.
+// Inf or NaN, tested on the bits (this file is built without NaN semantics).
+__device__ __forceinline__ bool nonfinite(float x) {
+    return (__float_as_uint(x) & 0x7f800000u) == 0x7f800000u;
+}
+
+// 2^x on the transcendental unit (inputs <= kTau; -inf gives 0).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Reductions over the four lanes {l, l^16, l^32, l^48} that hold one query:
@@ -68,14 +86,16 @@ __device__ __forceinline__ float quad_sum(float v) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-
-
 __global__ __launch_bounds__(256, 2) void k_attn_rank(
     const bf16* __restrict__ qkv, f16* __restrict__ out, int64_t row0, int H,
     const int32_t* __restrict__ hist_offsets, const int4* __restrict__ work,
-    const bf16* __restrict__ cache_k, const bf16* __restrict__ cache_v, int64_t cap) {
-    __shared__ __attribute__((aligned(16))) bf16 sK[2][kKS * kD];
-    __shared__ __attribute__((aligned(16))) bf16 sV[2][kD * kKS];   // transposed: [e][key col]
+    const bf16* __restrict__ cache_k, const bf16* __restrict__ cache_v, int64_t cap, float tau) {
+    // Stages as separate arrays: the compiler can then tell that reads of one
+    // stage do not alias the loads filling the other.
+    __shared__ __attribute__((aligned(16))) bf16 sK0[kKS * kD];
+    __shared__ __attribute__((aligned(16))) bf16 sK1[kKS * kD];
+    __shared__ __attribute__((aligned(16))) bf16 sV0[kKS * kD];
+    __shared__ __attribute__((aligned(16))) bf16 sV1[kKS * kD];
 
     const int4 item = work[blockIdx.x];
     const int u = item.x, h = item.y, kc = item.w;
@@ -86,160 +106,216 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
     const int d = H * kD;
     const int64_t hb = hist_offsets[u];
     const int n = hist_offsets[u + 1] - hist_offsets[u];
-    const bf16* Kh = cache_k + ((int64_t)h * cap + hb) * kD;
-    const bf16* Vh = cache_v + ((int64_t)h * cap + hb) * kD;
 
     // ---- queries of this wave (B operand of S^T), own key/value, initial state
     b8 qf[4][2];
-    float m[4], l[4];
-    f32x4 o[4][4];
+    f32x4 negm[4];                      // -m of the lane's query, in all four registers
+    float l[4];                         // lane-partial sums of probabilities
+    f32x4 o[4][4];                      // O^T: e = 16eb + 4g + r of query l16
+    // Loads the queries and starts the softmax from the candidate's own key
+    // and value, against reference max(own logit, mref[qg]) (mref = -inf:
+    // the own logit, so p_self = 1).
+    auto init_state = [&](const float (&mref)[4]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int qg = 0; qg < 4; ++qg) {
-        int qi = wave * kQW + qg * 16 + l16;
-        qi = qi < kc ? qi : kc - 1;                      // clamp the ragged tail
-        const bf16* qrow = qkv + (c0 - row0 + qi) * (int64_t)(3 * d) + h * kD;
-        const bf16* krow = qrow + d;
-        const bf16* vrow = qrow + 2 * d;
-        float s = 0.f;
+        for (int qg = 0; qg < 4; ++qg) {
+            int qi = wave * kQW + qg * 16 + l16;
+            qi = qi < kc ? qi : kc - 1;                  // clamp the ragged tail
+            const bf16* qrow = qkv + (c0 - row0 + qi) * (int64_t)(3 * d) + h * kD;
+            const bf16* krow = qrow + d;
+            const bf16* vrow = qrow + 2 * d;
+            float s = 0.f;
 #pragma unroll
-        for (int es = 0; es < 2; ++es) {
-            qf[qg][es] = *reinterpret_cast<const b8*>(qrow + es * 32 + 8 * g);
-            const b8 kf = *reinterpret_cast<const b8*>(krow + es * 32 + 8 * g);
+            for (int es = 0; es < 2; ++es) {
+                qf[qg][es] = *reinterpret_cast<const b8*>(qrow + es * 32 + 8 * g);
+                const b8 kf = *reinterpret_cast<const b8*>(krow + es * 32 + 8 * g);
 #pragma unroll
-            for (int j = 0; j < 8; ++j) s = fmaf((float)qf[qg][es][j], (float)kf[j], s);
+                for (int j = 0; j < 8; ++j) s = fmaf((float)qf[qg][es][j], (float)kf[j], s);
+            }
+            const float own = quad_sum(s);               // own logit
+            const float m0 = fmaxf(own, mref[qg]);
+            const float ps = fast_exp2(own - m0);        // 1 unless mref is larger
+            negm[qg] = f32x4{-m0, -m0, -m0, -m0};
+            l[qg] = g == 0 ? ps : 0.f;
+#pragma unroll
+            for (int eb = 0; eb < 4; ++eb) {
+                const bf16* vp = vrow + eb * 16 + 4 * g;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) o[qg][eb][r] = ps * (float)vp[r];
+            }
         }
-        m[qg] = quad_sum(s);                             // own logit
-        l[qg] = g == 0 ? 1.f : 0.f;                      // lane-partial sum
+    };
+    {
+        const float none[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        init_state(none);
+    }
+    float topmax = -INFINITY;           // lane maximum of s - m over all history
+
+    // ---- history K/V stages, loaded straight into LDS.  Buffer descriptors
+    // span the user's n rows, so rows past the history end read as zeros.
+    const int nst = (n + kKS - 1) / kKS;
+    const __amdgpu_buffer_rsrc_t rsK = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(cache_k + ((int64_t)h * cap + hb) * kD), (short)0, n * kD * 2, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rsV = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(cache_v + ((int64_t)h * cap + hb) * kD), (short)0, n * kD * 2, 0x00020000);
+    // Wave w fills rows 16w .. 16w+15 of a stage with two 8-row loads per
+    // matrix; slot s of row r holds logical chunk s ^ key(r).
+    int offK[2], offV[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int row = 16 * wave + 8 * i + (lane >> 3), slot = lane & 7;
+        offK[i] = row * kD * 2 + ((slot ^ key_k(row)) << 4);
+        offV[i] = row * kD * 2 + ((slot ^ key_v(row)) << 4);
+    }
+    auto issue_loads = [&](bf16* dK, bf16* dV, int st) __attribute__((always_inline)) {
+        const int base = st * kKS * kD * 2;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rsK, (__attribute__((address_space(3))) void*)(dK + (16 * wave + 8 * i) * kD),
+                16, offK[i] + base, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rsV, (__attribute__((address_space(3))) void*)(dV + (16 * wave + 8 * i) * kD),
+                16, offV[i] + base, 0, 0, 0);
+        }
+    };
+
+    // One 32-key sub-block (keys kb .. kb+31 of the stage in cK / cV).
+    auto sub_block = [&](const bf16* cK, const bf16* cV, int kb, int kabs) __attribute__((always_inline)) {
+        // S^T - m for 32 keys x 64 queries
+        f32x4 s[4][2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            b8 kf[2];
+            const int row = kb + t * 16 + l16;
+#pragma unroll
+            for (int es = 0; es < 2; ++es)
+                kf[es] = *reinterpret_cast<const b8*>(&cK[row * kD + (((es * 4 + g) ^ key_k(row)) << 3)]);
+#pragma unroll
+            for (int qg = 0; qg < 4; ++qg) {
+                f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[0], qf[qg][0], negm[qg], 0, 0, 0);
+                s[qg][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[1], qf[qg][1], acc, 0, 0, 0);
+            }
+        }
+        // mask keys past the history end (last sub-block only)
+        if (__builtin_expect(kabs + 32 > n, 0)) {
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const bool dead = kabs + t * 16 + 4 * g + r >= n;
+#pragma unroll
+                    for (int qg = 0; qg < 4; ++qg)
+                        if (dead) s[qg][t][r] = -INFINITY;
+                }
+        }
+        // lane maximum of s - m (no cross-lane step)
+        float top = max3(s[0][0][0], s[0][0][1], s[0][0][2]);
+#pragma unroll
+        for (int x = 3; x < 31; x += 2)
+            top = max3(top, s[x >> 3][(x >> 2) & 1][x & 3], s[(x + 1) >> 3][((x + 1) >> 2) & 1][(x + 1) & 3]);
+        top = fmaxf(top, s[3][1][3]);
+        b8 pf[4];
+#pragma unroll
+        for (int qg = 0; qg < 4; ++qg) {
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) pf[qg][t * 4 + r] = (__bf16)fast_exp2(s[qg][t][r]);
+            const b2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const b2 pp = {pf[qg][2 * j], pf[qg][2 * j + 1]};
+                l[qg] = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, l[qg], false);
+            }
+        }
+        // O^T += V^T P^T.  V^T fragment of e-block eb: lane (g, i) needs
+        // V[key(8g + j)][16eb + i]; in each 16-lane group, lane s of a
+        // transposing read addresses row 4g + s/4 (+16), dims 16eb + 4(s%4).
 #pragma unroll
         for (int eb = 0; eb < 4; ++eb) {
-            const bf16* vp = vrow + eb * 16 + 4 * g;
+            b8 vf;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) o[qg][eb][r] = (float)vp[r];
+            for (int hh = 0; hh < 2; ++hh) {
+                const int row = kb + 16 * hh + 4 * g + (l16 >> 2);
+                const int ch = 2 * eb + ((l16 & 3) >> 1);
+                const bf16* p = &cV[row * kD + ((ch ^ key_v(row)) << 3) + ((l16 & 1) << 2)];
+                const b4v v4 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                    (__attribute__((address_space(3))) b4v*)(p));
+#pragma unroll
+                for (int j = 0; j < 4; ++j) vf[4 * hh + j] = v4[j];
+            }
+#pragma unroll
+            for (int qg = 0; qg < 4; ++qg)
+                o[qg][eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qg], o[qg][eb], 0, 0, 0);
         }
-    }
+        topmax = fmaxf(topmax, top);
+    };
 
-    // ---- history K/V stages
-    const int nst = (n + kKS - 1) / kKS;
-    // K staging: thread loads 16-byte chunk (tid&7) of key rows tid>>3 and (tid>>3)+32.
-    // V staging: thread loads e-chunk (tid>>5) of keys 2*(tid&31) and 2*(tid&31)+1.
-    uint4 rk[2], rv[2];
-    auto gload = [&](int st) {
+    auto stage = [&](const bf16* cK, const bf16* cV, bf16* nK, bf16* nV, int st) __attribute__((always_inline)) {
+        if (st + 1 < nst) issue_loads(nK, nV, st + 1);
         const int k0 = st * kKS;
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int key = (tid >> 3) + 32 * i;
-            rk[i] = k0 + key < n ? *reinterpret_cast<const uint4*>(Kh + (int64_t)(k0 + key) * kD + (tid & 7) * 8)
-                                 : make_uint4(0, 0, 0, 0);
-            const int vkey = 2 * (tid & 31) + i;
-            rv[i] = k0 + vkey < n ? *reinterpret_cast<const uint4*>(Vh + (int64_t)(k0 + vkey) * kD + (tid >> 5) * 8)
-                                  : make_uint4(0, 0, 0, 0);
-        }
-    };
-    auto swrite = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int key = (tid >> 3) + 32 * i;
-            *reinterpret_cast<uint4*>(&sK[buf][swz(key, tid & 7)]) = rk[i];
-        }
-        // transpose V: (V[k][e], V[k+1][e]) -> one dword at column vcol(k) of row e
-        const int kk = 2 * (tid & 31), col = vcol(kk), e0 = (tid >> 5) * 8;
-        const uint32_t* a = reinterpret_cast<const uint32_t*>(&rv[0]);
-        const uint32_t* b = reinterpret_cast<const uint32_t*>(&rv[1]);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const uint32_t pair = __builtin_amdgcn_perm(b[j >> 1], a[j >> 1],
-                                                        (j & 1) ? 0x07060302u : 0x05040100u);
-            const int e = e0 + j;
-            *reinterpret_cast<uint32_t*>(&sV[buf][swz(e, col >> 3) + (col & 7)]) = pair;
-        }
+        sub_block(cK, cV, 0, k0);
+        if (k0 + 32 < n) sub_block(cK, cV, 32, k0 + 32);
+        __builtin_amdgcn_s_waitcnt(0x0F70);      // vmcnt(0): next stage landed
+        __syncthreads();
     };
 
-    if (nst > 0) {
-        gload(0);
-        swrite(0);
+    auto run = [&]() __attribute__((always_inline)) {
+        if (nst > 0) {
+            issue_loads(sK0, sV0, 0);
+            __builtin_amdgcn_s_waitcnt(0x0F70);
+        }
+        __syncthreads();
+        int st = 0;
+        for (; st + 2 <= nst; st += 2) {
+            stage(sK0, sV0, sK1, sV1, st);
+            stage(sK1, sV1, sK0, sV0, st + 1);
+        }
+        if (st < nst) stage(sK0, sV0, sK1, sV1, st);
+    };
+    run();
+
+    // ---- exact redo (pathological logit ranges only): if a logit exceeded
+    // its reference by more than kTau, or a sum overflowed, find each
+    // query's exact maximum logit over its history first, then run again
+    // against it, so no probability exceeds 1.
+    bool bad = topmax > tau;
+#pragma unroll
+    for (int qg = 0; qg < 4; ++qg) {
+        bad |= nonfinite(l[qg]);
+#pragma unroll
+        for (int eb = 0; eb < 4; ++eb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) bad |= nonfinite(o[qg][eb][r]);
     }
-    __syncthreads();
-    for (int st = 0; st < nst; ++st) {
-        const int buf = st & 1;
-        if (st + 1 < nst) gload(st + 1);
-#pragma unroll
-        for (int sub = 0; sub < 2; ++sub) {
-            const int kbase = st * kKS + sub * 32;
-            if (kbase >= n) break;
-            // S^T for 32 keys x 64 queries
-            f32x4 s[4][2];
-#pragma unroll
-            for (int t = 0; t < 2; ++t) {
+    if (__syncthreads_or(bad)) {
+        float mref[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        for (int st = 0; st < nst; ++st) {
+            issue_loads(sK0, sV0, st);
+            __builtin_amdgcn_s_waitcnt(0x0F70);
+            __syncthreads();
+            for (int kb = 0; kb < kKS && st * kKS + kb < n; kb += 16) {
                 b8 kf[2];
+                const int row = kb + l16;
 #pragma unroll
                 for (int es = 0; es < 2; ++es)
-                    kf[es] = *reinterpret_cast<const b8*>(&sK[buf][swz(sub * 32 + t * 16 + l16, es * 4 + g)]);
+                    kf[es] = *reinterpret_cast<const b8*>(&sK0[row * kD + (((es * 4 + g) ^ key_k(row)) << 3)]);
 #pragma unroll
                 for (int qg = 0; qg < 4; ++qg) {
                     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
                     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[0], qf[qg][0], acc, 0, 0, 0);
                     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[1], qf[qg][1], acc, 0, 0, 0);
-                    s[qg][t] = acc;
+                    float mx = -INFINITY;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (st * kKS + kb + 4 * g + r < n) mx = fmaxf(mx, acc[r]);
+                    mref[qg] = fmaxf(mref[qg], pair_max32(pair_max16(mx)));
                 }
             }
-            // mask keys past the history end (last sub-block only; kept off the
-            // steady-state path as an unlikely branch)
-            if (__builtin_expect(kbase + 32 > n, 0)) {
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const bool dead = kbase + t * 16 + 4 * g + r >= n;
-#pragma unroll
-                        for (int qg = 0; qg < 4; ++qg)
-                            if (dead) s[qg][t][r] = -INFINITY;
-                    }
-            }
-            // online softmax update
-            float alpha[4];
-            bool grew = false;
-            b8 pf[4];
-#pragma unroll
-            for (int qg = 0; qg < 4; ++qg) {
-                float mx = max3(s[qg][0][0], s[qg][0][1], s[qg][0][2]);
-                mx = max3(mx, s[qg][0][3], s[qg][1][0]);
-                mx = max3(mx, s[qg][1][1], s[qg][1][2]);
-                mx = fmaxf(mx, s[qg][1][3]);
-                mx = pair_max32(pair_max16(mx));
-                const float mn = fmaxf(m[qg], mx);
-                grew |= mn > m[qg];
-                alpha[qg] = fast_exp2(m[qg] - mn);
-                m[qg] = mn;
-                float sum = 0.f;
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const float p = fast_exp2(s[qg][t][r] - mn);
-                        sum += p;
-                        pf[qg][t * 4 + r] = (__bf16)p;
-                    }
-                l[qg] = fmaf(l[qg], alpha[qg], sum);
-            }
-            if (__any(grew)) {
-#pragma unroll
-                for (int qg = 0; qg < 4; ++qg)
-#pragma unroll
-                    for (int eb = 0; eb < 4; ++eb)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) o[qg][eb][r] *= alpha[qg];
-            }
-            // O^T += V^T P^T
-#pragma unroll
-            for (int eb = 0; eb < 4; ++eb) {
-                const b8 vf = *reinterpret_cast<const b8*>(&sV[buf][swz(eb * 16 + l16, sub * 4 + g)]);
-#pragma unroll
-                for (int qg = 0; qg < 4; ++qg)
-                    o[qg][eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qg], o[qg][eb], 0, 0, 0);
-            }
+            __syncthreads();
         }
-        if (st + 1 < nst) swrite(buf ^ 1);
-        __syncthreads();
+        init_state(mref);
+        run();
     }
 
     // ---- normalise and store (lane holds e = 16eb + 4g + r of query l16)
@@ -347,9 +423,16 @@ hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
     (void)cand_offsets;
     if (items == 0) return hipSuccess;
     if (D != kD || tile != kTQ) return hipErrorInvalidValue;
+    // UPR_ATTN_TAU lowers the headroom (testing: 0 sends nearly every work
+    // item through the exact two-pass redo)
+    float tau = kTau;
+    if (const char* e = std::getenv("UPR_ATTN_TAU")) {
+        const float v = std::strtof(e, nullptr);
+        if (v >= 0.f && v < kTau) tau = v;
+    }
     k_attn_rank<<<(unsigned)items, 256, 0, s>>>(qkv, o, row0, H, hist_offsets,
                                                 reinterpret_cast<const int4*>(work), cache_k,
-                                                cache_v, cache_cap);
+                                                cache_v, cache_cap, tau);
     return hipGetLastError();
 }
 

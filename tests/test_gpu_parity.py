@@ -77,6 +77,22 @@ def test_small_shapes_match_oracle(case, variant):
     _check_all(inp, f"small{case}/{variant}", score_scale=scale)
 
 
+@pytest.mark.parametrize("variant", ["perturbed", "sharp"])
+def test_exact_redo_path_matches_oracle(variant, monkeypatch):
+    """The ranking attention normally keeps each query's own logit as the
+    softmax reference; work items whose logits rise too far above it are
+    redone exactly (maximum logit first, then probabilities <= 1).  Headroom
+    0 sends nearly every work item through that redo, which must meet the
+    same bar."""
+    monkeypatch.setenv("UPR_ATTN_TAU", "0")
+    n, k, d, H, L, F, dt = SMALL[3]
+    scale = 1.0
+    if variant == "sharp":
+        L, scale = 1, 4.0
+    inp = make_inputs(n, k, d, H, L, F, dtype=dt, seed=321, variant=variant)
+    _check_all(inp, f"redo/{variant}", score_scale=scale)
+
+
 @pytest.mark.parametrize("name", ["tiny_f32", "u16_n256_k1000"])
 def test_named_workload_full_oracle(name):
     _check_all(make_workload(name, seed=0), name)

@@ -61,8 +61,8 @@ def kernel_work(inp):
 # Counter-measured HBM traffic per launch (profiles/traffic.json, written from
 # two rocprofv3 --pmc passes scaled by a plain-copy calibration).  A record
 # only applies while its kernel source is unchanged.
-TRAFFIC_KEYS = {"rank.attn": "k_attn_rank", "rank.gemm_qkv": "k_gemm_mfma<STORE(qkv)>",
-                "rank.gemm_up": "k_gemm_mfma<GELU(up)>"}
+TRAFFIC_KEYS = {"rank.attn": "attn", "rank.gemm_qkv": "gemm_qkv", "rank.gemm_up": "gemm_up",
+                "rank.gemm_o": "gemm_o", "rank.gemm_down": "gemm_down"}
 
 
 def measured_traffic(kernel, workload):

@@ -21,14 +21,14 @@
 // Softmax against a fixed reference: each query's reference logit m is its
 // own logit (p_self = 1, l = 1, O = v_self to start).  The logit MFMA
 // accumulates onto -m, giving s - m directly, and p = 2^(s - m) with no
-// running maximum and no rescaling of O: probabilities up to 2^kTau are
+// running maximum and no rescaling of O: probabilities above 1 are
 // accumulated as they are (fp32 sums, bf16 probabilities: relative precision
 // does not depend on magnitude), and the normaliser uses the same reference.
-// A work item in which some logit exceeds its reference by more than kTau
-// (a logit range no LayerNorm'd model produces) is redone exactly: a first
-// pass finds each query's maximum logit, and the second runs against it.
-// Row sums use v_dot2 over the bf16 probabilities, the same values that
-// weight V.
+// Only overflow can go wrong (a logit about 2^7 above its reference, a range
+// no LayerNorm'd model produces); a work item whose sums come out non-finite
+// is redone exactly: a first pass finds each query's maximum logit, and the
+// second runs against it.  Row sums use v_dot2 over the bf16 probabilities,
+// the same values that weight V.
 #include "upr_plan.h"
 
 #include <cstdlib>
@@ -46,7 +46,6 @@ constexpr int kD = 64;            // head_dim
 constexpr int kQW = 64;           // queries per wave
 constexpr int kTQ = 4 * kQW;      // queries per work item
 constexpr int kKS = 64;           // keys per LDS stage
-constexpr float kTau = 64.0f;     // log2 headroom above the softmax reference (maximum)
 static_assert(kTQ == kRankAttnTile, "work-list tile must match the kernel");
 
 // LDS layout of a stage: 64 rows (keys) x 128 bytes (64 dims), the eight
@@ -65,7 +64,7 @@ __device__ __forceinline__ bool nonfinite(float x) {
     return (__float_as_uint(x) & 0x7f800000u) == 0x7f800000u;
 }
 
-// 2^x on the transcendental unit (inputs <= kTau; -inf gives 0).
+// 2^x on the transcendental unit (-inf gives 0; 2^128 and above give inf).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Reductions over the four lanes {l, l^16, l^32, l^48} that hold one query:
@@ -89,7 +88,7 @@ __device__ __forceinline__ float quad_sum(float v) {
 __global__ __launch_bounds__(256, 2) void k_attn_rank(
     const bf16* __restrict__ qkv, f16* __restrict__ out, int64_t row0, int H,
     const int32_t* __restrict__ hist_offsets, const int4* __restrict__ work,
-    const bf16* __restrict__ cache_k, const bf16* __restrict__ cache_v, int64_t cap, float tau) {
+    const bf16* __restrict__ cache_k, const bf16* __restrict__ cache_v, int64_t cap, int force_exact) {
     // Stages as separate arrays: the compiler can then tell that reads of one
     // stage do not alias the loads filling the other.
     __shared__ __attribute__((aligned(16))) bf16 sK0[kKS * kD];
@@ -148,7 +147,6 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
         const float none[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
         init_state(none);
     }
-    float topmax = -INFINITY;           // lane maximum of s - m over all history
 
     // ---- history K/V stages, loaded straight into LDS.  Buffer descriptors
     // span the user's n rows, so rows past the history end read as zeros.
@@ -208,12 +206,6 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
                         if (dead) s[qg][t][r] = -INFINITY;
                 }
         }
-        // lane maximum of s - m (no cross-lane step)
-        float top = max3(s[0][0][0], s[0][0][1], s[0][0][2]);
-#pragma unroll
-        for (int x = 3; x < 31; x += 2)
-            top = max3(top, s[x >> 3][(x >> 2) & 1][x & 3], s[(x + 1) >> 3][((x + 1) >> 2) & 1][(x + 1) & 3]);
-        top = fmaxf(top, s[3][1][3]);
         b8 pf[4];
 #pragma unroll
         for (int qg = 0; qg < 4; ++qg) {
@@ -248,7 +240,6 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
             for (int qg = 0; qg < 4; ++qg)
                 o[qg][eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qg], o[qg][eb], 0, 0, 0);
         }
-        topmax = fmaxf(topmax, top);
     };
 
     auto stage = [&](const bf16* cK, const bf16* cV, bf16* nK, bf16* nV, int st) __attribute__((always_inline)) {
@@ -275,11 +266,11 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
     };
     run();
 
-    // ---- exact redo (pathological logit ranges only): if a logit exceeded
-    // its reference by more than kTau, or a sum overflowed, find each
+    // ---- exact redo (pathological logit ranges only): if a probability or
+    // a sum overflowed (a logit more than ~2^7 above its reference), find each
     // query's exact maximum logit over its history first, then run again
     // against it, so no probability exceeds 1.
-    bool bad = topmax > tau;
+    bool bad = force_exact != 0;
 #pragma unroll
     for (int qg = 0; qg < 4; ++qg) {
         bad |= nonfinite(l[qg]);
@@ -423,16 +414,13 @@ hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
     (void)cand_offsets;
     if (items == 0) return hipSuccess;
     if (D != kD || tile != kTQ) return hipErrorInvalidValue;
-    // UPR_ATTN_TAU lowers the headroom (testing: 0 sends nearly every work
-    // item through the exact two-pass redo)
-    float tau = kTau;
-    if (const char* e = std::getenv("UPR_ATTN_TAU")) {
-        const float v = std::strtof(e, nullptr);
-        if (v >= 0.f && v < kTau) tau = v;
-    }
+    // UPR_ATTN_EXACT=1 sends every work item through the exact two-pass redo
+    // (a testing hook for that path)
+    const char* e = std::getenv("UPR_ATTN_EXACT");
+    const int force_exact = e != nullptr && e[0] == '1';
     k_attn_rank<<<(unsigned)items, 256, 0, s>>>(qkv, o, row0, H, hist_offsets,
                                                 reinterpret_cast<const int4*>(work), cache_k,
-                                                cache_v, cache_cap, tau);
+                                                cache_v, cache_cap, force_exact);
     return hipGetLastError();
 }
 

@@ -21,7 +21,9 @@
 // instruction with 8-16 bytes each and reach about 60% of the bandwidth of
 // row-contiguous stores.  Each wave therefore stages its results through its
 // own LDS region, 32 rows at a time, and writes full 128-byte (16-bit output)
-// or 256-byte (fp32 residual) row segments, 16 bytes per lane.
+// or 256-byte (fp32 residual) row segments, 16 bytes per lane.  The stores
+// are non-temporal, so the output stream does not evict the operand panels
+// that later tiles re-read from L2.
 //
 // Tile order is XCD-aware: workgroup b runs on XCD b % 8 and the tiles are
 // renumbered so each XCD sweeps a contiguous range of (M-panel, N-tile)
@@ -36,6 +38,7 @@ namespace gemm_detail {
 typedef __attribute__((ext_vector_type(8))) _Float16 h8;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
 
 constexpr int kBM = 256, kBN = 256, kBK = 64;     // block tile
 constexpr int kThreads = 512;                      // 8 waves
@@ -275,7 +278,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict
                 if (row >= M || col >= N) continue;
                 float4 o = g[p];
                 o.x += x[p].x; o.y += x[p].y; o.z += x[p].z; o.w += x[p].w;
-                *reinterpret_cast<float4*>(epi.resid + row * epi.ldr + col) = o;
+                __builtin_nontemporal_store(f32x4{o.x, o.y, o.z, o.w}, reinterpret_cast<f32x4*>(epi.resid + row * epi.ldr + col));
             }
             __builtin_amdgcn_s_waitcnt(0xC07F);
             __builtin_amdgcn_wave_barrier();
@@ -354,7 +357,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict
                 } else {
                     dst = static_cast<unsigned short*>(epi.out) + row * epi.ldo + col;
                 }
-                *reinterpret_cast<u32x4*>(dst) = o;
+                __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(dst));
             }
             __builtin_amdgcn_s_waitcnt(0xC07F);
             __builtin_amdgcn_wave_barrier();

@@ -79,12 +79,11 @@ def test_small_shapes_match_oracle(case, variant):
 
 @pytest.mark.parametrize("variant", ["perturbed", "sharp"])
 def test_exact_redo_path_matches_oracle(variant, monkeypatch):
-    """The ranking attention normally keeps each query's own logit as the
-    softmax reference; work items whose logits rise too far above it are
-    redone exactly (maximum logit first, then probabilities <= 1).  Headroom
-    0 sends nearly every work item through that redo, which must meet the
-    same bar."""
-    monkeypatch.setenv("UPR_ATTN_TAU", "0")
+    """The ranking attention keeps each query's own logit as the softmax
+    reference; work items whose sums overflow are redone exactly (maximum
+    logit first, then probabilities <= 1).  UPR_ATTN_EXACT=1 sends every
+    work item through that redo, which must meet the same bar."""
+    monkeypatch.setenv("UPR_ATTN_EXACT", "1")
     n, k, d, H, L, F, dt = SMALL[3]
     scale = 1.0
     if variant == "sharp":

@@ -31,10 +31,11 @@ FLAGS = [
 ]
 
 
-# Extra flags per source.  The attention kernel's softmax takes maxima of
-# finite logits and -inf only; without NaN semantics each max is one
-# v_max3_f32 instead of a canonicalise-then-max pair.
-FILE_FLAGS = {"k_attn_rank.hip": ["-fno-honor-nans"]}
+# Extra flags per source.  The attention kernel takes maxima of finite logits
+# and -inf only (its overflow test reads the exponent bits); without NaN
+# semantics each max is one instruction instead of a canonicalise-then-max
+# pair.
+FILE_FLAGS = {"k_attn_mfma.hip": ["-fno-honor-nans"]}
 
 
 def sources():

@@ -1,25 +1,32 @@
-// Candidate cross-attention on the matrix cores (bf16, head_dim 64).
+// Attention on the matrix cores for bf16 models with head_dim 64: the
+// ranking pass (candidate cross-attention) and the encode pass (causal
+// history self-attention) share one kernel.
 //
-// For candidate c of user u and head h (paper Sec. 3: a candidate attends to
-// all of its user's history positions and to itself, never to another
-// candidate):  o_c = softmax([q_c . K_t]_t<n_u, q_c . k_c) [V; v_c],
-// with q pre-scaled by log2(e)/sqrt(D) so the softmax uses exp2.
+// Ranking (paper Sec. 3: a candidate attends to all of its user's history
+// positions and to itself, never to another candidate): for candidate c of
+// user u and head h,  o_c = softmax([q_c . K_t]_t<n_u, q_c . k_c) [V; v_c].
+// Encode (paper Eq. 2: causal attention over the history, diagonal
+// included): for history position i,  o_i = softmax([q_i . K_t]_t<=i) V.
+// Queries are pre-scaled by log2(e)/sqrt(D), so the softmax uses exp2.
 //
-// One workgroup = one work item (user, head, up to 256 candidates); four
-// waves of 64 candidates.  The user's cached K/V for this layer and head are
+// One workgroup = one work item (user, head, up to 256 query rows); four
+// waves of 64 queries.  The user's cached K/V for this layer and head are
 // streamed through LDS in 64-key stages (double-buffered, loaded straight
-// from global memory into LDS) and shared by all 256 candidates of the item.
-// Per 32-key sub-block each wave computes
+// from global memory into LDS) and shared by all queries of the item.  Per
+// 32-key sub-block each wave computes
 //   S^T = K Q^T        (v_mfma_f32_16x16x32_bf16, keys x queries),
 // so a lane holds 8 logits of ONE query (keys 4g..4g+3 and 16+4g..16+4g+3,
 // g = lane/16).  The probabilities, packed to bf16, are directly the B
 // operand of
 //   O^T += V^T P^T     (e x queries);
 // V stays row-major in LDS and the transposing LDS read (ds_read_b64_tr_b16)
-// delivers V^T fragments in that same key order.
+// delivers V^T fragments in that same key order.  In the causal pass a wave
+// skips sub-blocks that lie entirely after its last query and masks the
+// diagonal ones.
 //
 // Softmax against a fixed reference: each query's reference logit m is its
-// own logit (p_self = 1, l = 1, O = v_self to start).  The logit MFMA
+// own logit q . k_self (ranking: p_self = 1, l = 1, O = v_self to start;
+// encode: the diagonal key is one of the streamed keys).  The logit MFMA
 // accumulates onto -m, giving s - m directly, and p = 2^(s - m) with no
 // running maximum and no rescaling of O: probabilities above 1 are
 // accumulated as they are (fp32 sums, bf16 probabilities: relative precision
@@ -46,7 +53,7 @@ constexpr int kD = 64;            // head_dim
 constexpr int kQW = 64;           // queries per wave
 constexpr int kTQ = 4 * kQW;      // queries per work item
 constexpr int kKS = 64;           // keys per LDS stage
-static_assert(kTQ == kRankAttnTile, "work-list tile must match the kernel");
+static_assert(kTQ == kAttnTile, "work-list tile must match the kernel");
 
 // LDS layout of a stage: 64 rows (keys) x 128 bytes (64 dims), the eight
 // 16-byte chunks of a row XOR-swizzled.  K fragment reads take 16
@@ -85,8 +92,12 @@ __device__ __forceinline__ float quad_sum(float v) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-__global__ __launch_bounds__(256, 2) void k_attn_rank(
-    const bf16* __restrict__ qkv, f16* __restrict__ out, int64_t row0, int H,
+// CAUSAL = false: ranking; queries are candidate rows of qsrc = q|k|v rows
+// (stride 3d, own key and value at +d, +2d).  CAUSAL = true: encode; queries
+// are history rows of qsrc = query rows (stride d), own keys in the cache.
+template <bool CAUSAL>
+__global__ __launch_bounds__(256, 2) void k_attn_mfma(
+    const bf16* __restrict__ qsrc, int64_t qstride, f16* __restrict__ out, int64_t row0, int H,
     const int32_t* __restrict__ hist_offsets, const int4* __restrict__ work,
     const bf16* __restrict__ cache_k, const bf16* __restrict__ cache_v, int64_t cap, int force_exact) {
     // Stages as separate arrays: the compiler can then tell that reads of one
@@ -99,29 +110,37 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
     const int4 item = work[blockIdx.x];
     const int u = item.x, h = item.y, kc = item.w;
     if (kc <= 0) return;
-    const int64_t c0 = item.z;          // absolute first candidate row
+    const int64_t c0 = item.z;          // absolute row of the first query
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, l16 = lane & 15;
     const int d = H * kD;
     const int64_t hb = hist_offsets[u];
     const int n = hist_offsets[u + 1] - hist_offsets[u];
+    // keys streamed: all history (ranking) or positions up to the item's
+    // last query (encode); waves past the item's queries only help load
+    const int ipos0 = CAUSAL ? (int)(c0 - hb) : 0;
+    const int nkeys = CAUSAL ? ipos0 + kc : n;
+    const bool wave_active = wave * kQW < kc;
+    const int wave_last = ipos0 + min(wave * kQW + kQW, kc) - 1;   // encode: last query position
 
     // ---- queries of this wave (B operand of S^T), own key/value, initial state
     b8 qf[4][2];
     f32x4 negm[4];                      // -m of the lane's query, in all four registers
     float l[4];                         // lane-partial sums of probabilities
     f32x4 o[4][4];                      // O^T: e = 16eb + 4g + r of query l16
-    // Loads the queries and starts the softmax from the candidate's own key
-    // and value, against reference max(own logit, mref[qg]) (mref = -inf:
-    // the own logit, so p_self = 1).
+    // Loads the queries and starts the softmax against reference
+    // max(own logit, mref[qg]) (mref = -inf: the own logit).  Ranking starts
+    // from the candidate's own key and value (p_self = 1 against its own
+    // logit); encode from nothing (the diagonal key is streamed).
+    int qpos[4];                        // encode: position of the lane's query
     auto init_state = [&](const float (&mref)[4]) __attribute__((always_inline)) {
 #pragma unroll
         for (int qg = 0; qg < 4; ++qg) {
             int qi = wave * kQW + qg * 16 + l16;
             qi = qi < kc ? qi : kc - 1;                  // clamp the ragged tail
-            const bf16* qrow = qkv + (c0 - row0 + qi) * (int64_t)(3 * d) + h * kD;
-            const bf16* krow = qrow + d;
-            const bf16* vrow = qrow + 2 * d;
+            qpos[qg] = ipos0 + qi;
+            const bf16* qrow = qsrc + (c0 - row0 + qi) * qstride + h * kD;
+            const bf16* krow = CAUSAL ? cache_k + ((int64_t)h * cap + c0 + qi) * kD : qrow + d;
             float s = 0.f;
 #pragma unroll
             for (int es = 0; es < 2; ++es) {
@@ -134,12 +153,19 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
             const float m0 = fmaxf(own, mref[qg]);
             const float ps = fast_exp2(own - m0);        // 1 unless mref is larger
             negm[qg] = f32x4{-m0, -m0, -m0, -m0};
-            l[qg] = g == 0 ? ps : 0.f;
+            if constexpr (CAUSAL) {
+                l[qg] = 0.f;
 #pragma unroll
-            for (int eb = 0; eb < 4; ++eb) {
-                const bf16* vp = vrow + eb * 16 + 4 * g;
+                for (int eb = 0; eb < 4; ++eb) o[qg][eb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            } else {
+                l[qg] = g == 0 ? ps : 0.f;
+                const bf16* vrow = qrow + 2 * d;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) o[qg][eb][r] = ps * (float)vp[r];
+                for (int eb = 0; eb < 4; ++eb) {
+                    const bf16* vp = vrow + eb * 16 + 4 * g;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) o[qg][eb][r] = ps * (float)vp[r];
+                }
             }
         }
     };
@@ -150,7 +176,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
 
     // ---- history K/V stages, loaded straight into LDS.  Buffer descriptors
     // span the user's n rows, so rows past the history end read as zeros.
-    const int nst = (n + kKS - 1) / kKS;
+    const int nst = (nkeys + kKS - 1) / kKS;
     const __amdgpu_buffer_rsrc_t rsK = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(cache_k + ((int64_t)h * cap + hb) * kD), (short)0, n * kD * 2, 0x00020000);
     const __amdgpu_buffer_rsrc_t rsV = __builtin_amdgcn_make_buffer_rsrc(
@@ -179,6 +205,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
 
     // One 32-key sub-block (keys kb .. kb+31 of the stage in cK / cV).
     auto sub_block = [&](const bf16* cK, const bf16* cV, int kb, int kabs) __attribute__((always_inline)) {
+        if (!wave_active || (CAUSAL && kabs > wave_last)) return;   // nothing to do for this wave
         // S^T - m for 32 keys x 64 queries
         f32x4 s[4][2];
 #pragma unroll
@@ -194,16 +221,17 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
                 s[qg][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[1], qf[qg][1], acc, 0, 0, 0);
             }
         }
-        // mask keys past the history end (last sub-block only)
-        if (__builtin_expect(kabs + 32 > n, 0)) {
+        // ranking: mask keys past the history end (last sub-block only);
+        // encode: mask keys after the query (diagonal sub-blocks only)
+        if (__builtin_expect(CAUSAL ? kabs + 31 > ipos0 + wave * kQW : kabs + 32 > n, 0)) {
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const bool dead = kabs + t * 16 + 4 * g + r >= n;
+                    const int key = kabs + t * 16 + 4 * g + r;
 #pragma unroll
                     for (int qg = 0; qg < 4; ++qg)
-                        if (dead) s[qg][t][r] = -INFINITY;
+                        if (CAUSAL ? key > qpos[qg] : key >= n) s[qg][t][r] = -INFINITY;
                 }
         }
         b8 pf[4];
@@ -246,7 +274,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
         if (st + 1 < nst) issue_loads(nK, nV, st + 1);
         const int k0 = st * kKS;
         sub_block(cK, cV, 0, k0);
-        if (k0 + 32 < n) sub_block(cK, cV, 32, k0 + 32);
+        if (k0 + 32 < nkeys) sub_block(cK, cV, 32, k0 + 32);
         __builtin_amdgcn_s_waitcnt(0x0F70);      // vmcnt(0): next stage landed
         __syncthreads();
     };
@@ -285,7 +313,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
             issue_loads(sK0, sV0, st);
             __builtin_amdgcn_s_waitcnt(0x0F70);
             __syncthreads();
-            for (int kb = 0; kb < kKS && st * kKS + kb < n; kb += 16) {
+            for (int kb = 0; kb < kKS && st * kKS + kb < nkeys; kb += 16) {
                 b8 kf[2];
                 const int row = kb + l16;
 #pragma unroll
@@ -298,8 +326,10 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
                     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[1], qf[qg][1], acc, 0, 0, 0);
                     float mx = -INFINITY;
 #pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        if (st * kKS + kb + 4 * g + r < n) mx = fmaxf(mx, acc[r]);
+                    for (int r = 0; r < 4; ++r) {
+                        const int key = st * kKS + kb + 4 * g + r;
+                        if (CAUSAL ? key <= qpos[qg] : key < n) mx = fmaxf(mx, acc[r]);
+                    }
                     mref[qg] = fmaxf(mref[qg], pair_max32(pair_max16(mx)));
                 }
             }
@@ -331,14 +361,17 @@ __global__ __launch_bounds__(256, 2) void k_attn_rank(
 // Work list: users ordered by history length (longest first, ties by index)
 // when there are at most kSortMax users, else in index order.  Items of user
 // u (rank r) occupy H * start_r .. H * (start_r + tiles_u) - 1, item
-// H*(start_r + t) + h being tile t of head h, so with H = 8 all tiles of one
-// (user, head) share blockIdx % 8 and therefore one XCD's L2.
+// H*(start_r + j) + h being tile j of head h (tile tiles_u - 1 - j when
+// `reverse`: the causal pass puts a user's costliest, last tiles first), so
+// with H = 8 all tiles of one (user, head) share blockIdx % 8 and therefore
+// one XCD's L2.  Tiles cover the rows of `coffs` (candidates, or the history
+// itself for the causal pass).
 constexpr int kSortMax = 2048;
 
 __global__ __launch_bounds__(1024) void k_rank_worklist(const int32_t* __restrict__ coffs,
                                                         const int32_t* __restrict__ hoffs, int U,
-                                                        int H, int tile, int4* __restrict__ work,
-                                                        int64_t items) {
+                                                        int H, int tile, int reverse,
+                                                        int4* __restrict__ work, int64_t items) {
     __shared__ int s_len[kSortMax];
     __shared__ int s_tiles[kSortMax];     // tiles of the user at each rank
     __shared__ int s_user[kSortMax];      // user at each rank
@@ -386,8 +419,9 @@ __global__ __launch_bounds__(1024) void k_rank_worklist(const int32_t* __restric
                 for (int hh = 0; hh < H; ++hh) {
                     const long long idx = (long long)H * (start + j) + hh;
                     if (idx < items) {
-                        const int cnt = min(tile, k - j * tile);
-                        work[idx] = make_int4(u, hh, coffs[u] + j * tile, cnt);
+                        const int tt = reverse ? t - 1 - j : j;
+                        const int cnt = min(tile, k - tt * tile);
+                        work[idx] = make_int4(u, hh, coffs[u] + tt * tile, cnt);
                     }
                 }
         }
@@ -399,28 +433,43 @@ __global__ __launch_bounds__(1024) void k_rank_worklist(const int32_t* __restric
 
 }  // namespace
 
-hipError_t launch_rank_worklist(const int32_t* cand_offsets, const int32_t* hist_offsets, int U,
-                                int H, int tile, int32_t* work, int64_t items, hipStream_t s) {
+hipError_t launch_attn_worklist(const int32_t* row_offsets, const int32_t* hist_offsets, int U,
+                                int H, int tile, bool reverse, int32_t* work, int64_t items,
+                                hipStream_t s) {
     if (items == 0) return hipSuccess;
-    k_rank_worklist<<<1, 1024, 0, s>>>(cand_offsets, hist_offsets, U, H, tile,
+    k_rank_worklist<<<1, 1024, 0, s>>>(row_offsets, hist_offsets, U, H, tile, reverse ? 1 : 0,
                                        reinterpret_cast<int4*>(work), items);
     return hipGetLastError();
 }
 
+// UPR_ATTN_EXACT=1 sends every work item through the exact two-pass redo (a
+// testing hook for that path).
+static int force_exact_flag() {
+    const char* e = std::getenv("UPR_ATTN_EXACT");
+    return e != nullptr && e[0] == '1';
+}
+
 hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
-                            const int32_t* cand_offsets, const int32_t* hist_offsets,
-                            const int32_t* work, int64_t items, int tile, const bf16* cache_k,
-                            const bf16* cache_v, int64_t cache_cap, hipStream_t s) {
-    (void)cand_offsets;
+                            const int32_t* hist_offsets, const int32_t* work, int64_t items,
+                            int tile, const bf16* cache_k, const bf16* cache_v, int64_t cache_cap,
+                            hipStream_t s) {
     if (items == 0) return hipSuccess;
     if (D != kD || tile != kTQ) return hipErrorInvalidValue;
-    // UPR_ATTN_EXACT=1 sends every work item through the exact two-pass redo
-    // (a testing hook for that path)
-    const char* e = std::getenv("UPR_ATTN_EXACT");
-    const int force_exact = e != nullptr && e[0] == '1';
-    k_attn_rank<<<(unsigned)items, 256, 0, s>>>(qkv, o, row0, H, hist_offsets,
-                                                reinterpret_cast<const int4*>(work), cache_k,
-                                                cache_v, cache_cap, force_exact);
+    k_attn_mfma<false><<<(unsigned)items, 256, 0, s>>>(
+        qkv, (int64_t)3 * H * kD, o, row0, H, hist_offsets, reinterpret_cast<const int4*>(work),
+        cache_k, cache_v, cache_cap, force_exact_flag());
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_encode(const bf16* q, f16* o, int64_t row0, int H, int D,
+                              const int32_t* hist_offsets, const int32_t* work, int64_t items,
+                              int tile, const bf16* cache_k, const bf16* cache_v,
+                              int64_t cache_cap, hipStream_t s) {
+    if (items == 0) return hipSuccess;
+    if (D != kD || tile != kTQ) return hipErrorInvalidValue;
+    k_attn_mfma<true><<<(unsigned)items, 256, 0, s>>>(
+        q, (int64_t)H * kD, o, row0, H, hist_offsets, reinterpret_cast<const int4*>(work), cache_k,
+        cache_v, cache_cap, force_exact_flag());
     return hipGetLastError();
 }
 

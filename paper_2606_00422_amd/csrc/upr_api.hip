@@ -206,6 +206,11 @@ static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_
     UPR_LAUNCH("encode.init_ln1",
                launch_init_layernorm<T, TA>(hist_emb + p.row0 * d, g, a, R, d, m->layers[0].ln1_g,
                                             m->layers[0].ln1_b, c.ln_eps, s));
+    if (p.use_mfma_attn && c.n_layers > 1)
+        UPR_LAUNCH("encode.worklist",
+                   launch_attn_worklist(hist->offsets_dev, hist->offsets_dev, hist->num_users, H,
+                                        p.attn_tile, true, reinterpret_cast<int32_t*>(ws + p.off_work),
+                                        p.work_items, s));
     for (int l = 0; l < c.n_layers; ++l) {
         const LayerWeights& w = m->layers[l];
         if (l > 0)
@@ -228,11 +233,26 @@ static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_
         UPR_LAUNCH("encode.gemm_qkv",
                    launch_gemm<TA, T>(a, d, static_cast<const TA*>(w.Wqkv), R, 3 * d, d, e, s));
         if (l == c.n_layers - 1) break;     // the cache is complete; nothing reads further
-        UPR_LAUNCH("encode.attn", launch_attn_encode_simple<T, TA>(q, o, R, p.row0, H, D, hist->offsets_dev,
-                                             hist->num_users,
-                                             static_cast<const T*>(e.cache_k),
-                                             static_cast<const T*>(e.cache_v),
-                                             cache->capacity_rows, s));
+        bool done = false;
+        if constexpr (std::is_same_v<Types, Bf16Types>) {
+            if (p.use_mfma_attn) {
+                UPR_LAUNCH("encode.attn",
+                           launch_attn_encode(q, o, p.row0, H, D, hist->offsets_dev,
+                                              reinterpret_cast<const int32_t*>(ws + p.off_work),
+                                              p.work_items, p.attn_tile,
+                                              static_cast<const T*>(e.cache_k),
+                                              static_cast<const T*>(e.cache_v),
+                                              cache->capacity_rows, s));
+                done = true;
+            }
+        }
+        if (!done)
+            UPR_LAUNCH("encode.attn",
+                       launch_attn_encode_simple<T, TA>(q, o, R, p.row0, H, D, hist->offsets_dev,
+                                                        hist->num_users,
+                                                        static_cast<const T*>(e.cache_k),
+                                                        static_cast<const T*>(e.cache_v),
+                                                        cache->capacity_rows, s));
         UPR_HIP(launch_ffn_block<Types>(kEncodeFfnNames, w, o, a, h, g, R, d, F, c.ln_eps, s));
     }
     return UPR_OK;
@@ -258,8 +278,8 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
                launch_init_layernorm<T, TA>(cand_emb + p.row0 * d, g, a, R, d, m->layers[0].ln1_g,
                                             m->layers[0].ln1_b, c.ln_eps, s));
     if (p.use_mfma_attn)
-        UPR_LAUNCH("rank.worklist", launch_rank_worklist(cand->offsets_dev, hist->offsets_dev, cand->num_users, H,
-                                     p.attn_tile, reinterpret_cast<int32_t*>(ws + p.off_work),
+        UPR_LAUNCH("rank.worklist", launch_attn_worklist(cand->offsets_dev, hist->offsets_dev, cand->num_users, H,
+                                     p.attn_tile, false, reinterpret_cast<int32_t*>(ws + p.off_work),
                                      p.work_items, s));
     for (int l = 0; l < c.n_layers; ++l) {
         const LayerWeights& w = m->layers[l];
@@ -280,8 +300,7 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
         bool done = false;
         if constexpr (std::is_same_v<Types, Bf16Types>) {
             if (p.use_mfma_attn) {
-                UPR_LAUNCH("rank.attn", launch_attn_rank(qkv, o, p.row0, H, D, cand->offsets_dev,
-                                         hist->offsets_dev,
+                UPR_LAUNCH("rank.attn", launch_attn_rank(qkv, o, p.row0, H, D, hist->offsets_dev,
                                          reinterpret_cast<const int32_t*>(ws + p.off_work),
                                          p.work_items, p.attn_tile, ck, cv, cache->capacity_rows,
                                          s));
@@ -477,7 +496,7 @@ size_t upr_encode_workspace_bytes(const upr_model* m, const upr_segments* hist) 
     if (!m) return 0;
     int64_t first, last;
     if (check_segments(hist, "hist", &first, &last) != UPR_OK) return 0;
-    return upr::plan_encode(m->cfg, first, last).bytes;
+    return upr::plan_encode(m->cfg, hist->num_users, hist->offsets_host).bytes;
 }
 
 size_t upr_rank_workspace_bytes(const upr_model* m, const upr_segments* hist,
@@ -502,7 +521,7 @@ upr_status upr_encode_user(const upr_model* m, const void* hist_emb, const upr_s
     if (cache->capacity_rows < 0 || last > cache->capacity_rows)
         return fail(UPR_ERR_CAPACITY, "history rows end at %lld, cache capacity is %lld",
                     (long long)last, (long long)cache->capacity_rows);
-    const upr::EncodePlan p = upr::plan_encode(m->cfg, first, last);
+    const upr::EncodePlan p = upr::plan_encode(m->cfg, hist->num_users, hist->offsets_host);
     st = check_workspace(ws, ws_bytes, p.bytes);
     if (st != UPR_OK) return st;
     if (p.rows == 0) return ok();

@@ -10,14 +10,17 @@ namespace upr {
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// Candidates per work item of the MFMA ranking attention (one workgroup
-// handles this many candidates of one user for one head).
-constexpr int kRankAttnTile = 256;
-constexpr bool kHaveMfmaRankAttn = true;
+// Query rows per work item of the MFMA attention (one workgroup handles this
+// many candidates, or history rows, of one user for one head).
+constexpr int kAttnTile = 256;
+constexpr bool kHaveMfmaAttn = true;
 
 struct EncodePlan {
     int64_t row0 = 0, rows = 0;
-    size_t off_g = 0, off_a = 0, off_q = 0, off_o = 0, off_h = 0;
+    size_t off_g = 0, off_a = 0, off_q = 0, off_o = 0, off_h = 0, off_work = 0;
+    int64_t work_items = 0;
+    int attn_tile = kAttnTile;
+    bool use_mfma_attn = false;
     size_t bytes = 0;
 };
 
@@ -25,27 +28,43 @@ struct RankPlan {
     int64_t row0 = 0, rows = 0;
     size_t off_g = 0, off_a = 0, off_qkv = 0, off_o = 0, off_h = 0, off_work = 0;
     int64_t work_items = 0;
-    int attn_tile = kRankAttnTile;
+    int attn_tile = kAttnTile;
     bool use_mfma_attn = false;
     size_t bytes = 0;
 };
 
 inline size_t dtype_bytes(const upr_config& c) { return c.dtype == UPR_BF16 ? 2 : 4; }
 
-// Workspace of encode for history rows [first, last): fp32 residual stream,
-// then LayerNorm output, queries, attention output and FFN hidden (model dtype).
-inline EncodePlan plan_encode(const upr_config& c, int64_t first, int64_t last) {
+// Number of MFMA attention work items over the rows of `offs`: one per
+// (user, head, tile of up to kAttnTile rows).
+inline int64_t attn_items(const upr_config& c, int U, const int32_t* offs) {
+    int64_t items = 0;
+    for (int u = 0; u < U; ++u) items += ((int64_t)offs[u + 1] - offs[u] + kAttnTile - 1) / kAttnTile;
+    return items * c.n_heads;
+}
+
+inline bool use_mfma_attn(const upr_config& c) {
+    return kHaveMfmaAttn && c.dtype == UPR_BF16 && c.head_dim == 64;
+}
+
+// Workspace of encode for the history rows of `hoffs` (host offsets): fp32
+// residual stream, then LayerNorm output, queries, attention output and FFN
+// hidden (model dtype), and (bf16 models) the attention work list.
+inline EncodePlan plan_encode(const upr_config& c, int U, const int32_t* hoffs) {
     EncodePlan p;
-    p.row0 = first;
-    p.rows = last - first;
+    p.row0 = hoffs[0];
+    p.rows = (int64_t)hoffs[U] - hoffs[0];
     if (p.rows <= 0) { p.rows = 0; return p; }
     const size_t es = dtype_bytes(c), R = (size_t)p.rows, d = c.d_model, F = c.d_ff;
+    p.use_mfma_attn = use_mfma_attn(c);
+    if (p.use_mfma_attn) p.work_items = attn_items(c, U, hoffs);
     size_t o = 0;
     p.off_g = o; o = align256(o + R * d * 4);
     p.off_a = o; o = align256(o + R * d * es);
     p.off_q = o; o = align256(o + R * d * es);
     p.off_o = o; o = align256(o + R * d * es);
     p.off_h = o; o = align256(o + R * F * es);
+    p.off_work = o; o = align256(o + (size_t)p.work_items * 4 * sizeof(int32_t));
     p.bytes = o;
     return p;
 }
@@ -59,15 +78,8 @@ inline RankPlan plan_rank(const upr_config& c, int U, const int32_t* coffs) {
     p.rows = (int64_t)coffs[U] - coffs[0];
     if (p.rows <= 0) { p.rows = 0; return p; }
     const size_t es = dtype_bytes(c), R = (size_t)p.rows, d = c.d_model, F = c.d_ff;
-    p.use_mfma_attn = kHaveMfmaRankAttn && c.dtype == UPR_BF16 && c.head_dim == 64;
-    if (p.use_mfma_attn) {
-        int64_t items = 0;
-        for (int u = 0; u < U; ++u) {
-            const int64_t k = (int64_t)coffs[u + 1] - coffs[u];
-            items += (k + p.attn_tile - 1) / p.attn_tile;
-        }
-        p.work_items = items * c.n_heads;
-    }
+    p.use_mfma_attn = use_mfma_attn(c);
+    if (p.use_mfma_attn) p.work_items = attn_items(c, U, coffs);
     size_t o = 0;
     p.off_g = o; o = align256(o + R * d * 4);
     p.off_a = o; o = align256(o + R * d * es);
@@ -89,15 +101,25 @@ hipError_t launch_gemm(const TA* A, int64_t lda, const TA* W, int64_t M, int N, 
 hipError_t launch_gemm_mfma(const f16* A, int64_t lda, const f16* W, int64_t M, int N, int K,
                             const Epilogue& epi, hipStream_t s);
 
-// Work list of the MFMA ranking attention: entries (user, head, first
-// candidate row, candidate count), heaviest users first.
-hipError_t launch_rank_worklist(const int32_t* cand_offsets, const int32_t* hist_offsets, int U,
-                                int H, int tile, int32_t* work, int64_t items, hipStream_t s);
+// Work list of the MFMA attention: entries (user, head, first query row,
+// query count) over the rows of `row_offsets` (candidates, or the history
+// itself for encode), users with the longest history first; `reverse` lists
+// each user's tiles last-first (encode: the costliest causal tiles first).
+hipError_t launch_attn_worklist(const int32_t* row_offsets, const int32_t* hist_offsets, int U,
+                                int H, int tile, bool reverse, int32_t* work, int64_t items,
+                                hipStream_t s);
 
-// MFMA ranking attention (bf16 queries/cache, head_dim 64), fp16 output.
+// MFMA ranking attention (bf16 q|k|v rows and cache, head_dim 64), fp16 output.
 hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
-                            const int32_t* cand_offsets, const int32_t* hist_offsets,
-                            const int32_t* work, int64_t items, int tile, const bf16* cache_k,
-                            const bf16* cache_v, int64_t cache_cap, hipStream_t s);
+                            const int32_t* hist_offsets, const int32_t* work, int64_t items,
+                            int tile, const bf16* cache_k, const bf16* cache_v, int64_t cache_cap,
+                            hipStream_t s);
+
+// MFMA causal encode attention (bf16 query rows and cache, head_dim 64),
+// fp16 output.
+hipError_t launch_attn_encode(const bf16* q, f16* o, int64_t row0, int H, int D,
+                              const int32_t* hist_offsets, const int32_t* work, int64_t items,
+                              int tile, const bf16* cache_k, const bf16* cache_v,
+                              int64_t cache_cap, hipStream_t s);
 
 }  // namespace upr

@@ -71,12 +71,13 @@ __device__ __forceinline__ int swz(int row, int chunk) {
 }
 
 // GELU, tanh form, as x * sigmoid(2y) with y = sqrt(2/pi) (x + 0.044715 x^3):
-// 0.5 x (1 + tanh(y)) = x / (1 + exp(-2y)).
+// 0.5 x (1 + tanh(y)) = x / (1 + 2^(-2 log2(e) y)), the exponent folded to
+// x (c1 + c2 x^2).
 __device__ __forceinline__ float gelu_fast(float x) {
-    const float x2 = x * x;
-    const float u = fmaf(0.044715f * x2, x, x);                  // x + 0.044715 x^3
-    const float z = -2.0f * 1.4426950408889634f * 0.7978845608028654f * u;
-    return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z));
+    constexpr float c1 = -2.0f * 1.4426950408889634f * 0.7978845608028654f;
+    constexpr float c2 = c1 * 0.044715f;
+    const float t = fmaf(c2, x * x, c1);
+    return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * t));
 }
 
 // Two values rounded to bf16 (BF) or fp16, packed low-first.
@@ -91,6 +92,156 @@ __device__ __forceinline__ unsigned pack2(float a, float b) {
         y = __builtin_bit_cast(unsigned short, (_Float16)keep_f32(b));
     }
     return (unsigned)x | ((unsigned)y << 16);
+}
+
+// Epilogue of one wave's 128 x 64 tile (acc in the transposed MFMA layout:
+// register r of tile (j, i) holds row 32i + lane%32 and column
+// 32j + 8(r/4) + 4(lane/32) + r%4 of the wave tile at (wrow0, wcol0)),
+// staged through the wave's own LDS region (fp32 residual passes of RROWS
+// rows: RROWS x 272 bytes; 16-bit passes of 32 rows: 32 x 144 bytes).
+template <int MODE, int RROWS>
+__device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* const region,
+                                           int64_t wrow0, int wcol0, int64_t M, int N,
+                                           const Epilogue& epi, int lane) {
+    const int lrow = lane & 31, lhalf = lane >> 5;
+    float4 bq[kTN][4];
+#pragma unroll
+    for (int j = 0; j < kTN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int col = wcol0 + j * 32 + 8 * q + 4 * lhalf;
+            bq[j][q] = col < N ? *reinterpret_cast<const float4*>(epi.bias + col)
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    const float sc = epi.acc_scale;
+
+    if constexpr (MODE == EPI_RESID) {
+        // fp32 staging: a lane writes its four-column runs (16 bytes); reads
+        // give 16 lanes per 256-byte row segment, 4 rows per instruction.
+        float* const st = reinterpret_cast<float*>(region);
+        const int ch = lane & 15;
+        const int col = wcol0 + ch * 4;
+        constexpr int kPasses = 32 / RROWS;
+#pragma unroll
+        for (int i = 0; i < kTM; ++i) {
+#pragma unroll
+            for (int hp = 0; hp < kPasses; ++hp) {
+                if (lrow / RROWS == hp) {
+#pragma unroll
+                    for (int j = 0; j < kTN; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            float4 v;
+                            v.x = fmaf(acc[j][i][4 * q + 0], sc, bq[j][q].x);
+                            v.y = fmaf(acc[j][i][4 * q + 1], sc, bq[j][q].y);
+                            v.z = fmaf(acc[j][i][4 * q + 2], sc, bq[j][q].z);
+                            v.w = fmaf(acc[j][i][4 * q + 3], sc, bq[j][q].w);
+                            *reinterpret_cast<float4*>(st + (lrow % RROWS) * kStage32 + j * 32 + 8 * q + 4 * lhalf) = v;
+                        }
+                }
+                __builtin_amdgcn_s_waitcnt(0xC07F);
+                __builtin_amdgcn_wave_barrier();
+                float4 x[RROWS / 4], g[RROWS / 4];
+#pragma unroll
+                for (int p = 0; p < RROWS / 4; ++p) {
+                    const int rl = p * 4 + (lane >> 4);
+                    const int64_t row = wrow0 + i * 32 + hp * RROWS + rl;
+                    x[p] = *reinterpret_cast<const float4*>(st + rl * kStage32 + ch * 4);
+                    if (row < M && col < N)
+                        g[p] = *reinterpret_cast<const float4*>(epi.resid + row * epi.ldr + col);
+                }
+#pragma unroll
+                for (int p = 0; p < RROWS / 4; ++p) {
+                    const int64_t row = wrow0 + i * 32 + hp * RROWS + p * 4 + (lane >> 4);
+                    if (row >= M || col >= N) continue;
+                    float4 o = g[p];
+                    o.x += x[p].x; o.y += x[p].y; o.z += x[p].z; o.w += x[p].w;
+                    __builtin_nontemporal_store(f32x4{o.x, o.y, o.z, o.w}, reinterpret_cast<f32x4*>(epi.resid + row * epi.ldr + col));
+                }
+                __builtin_amdgcn_s_waitcnt(0xC07F);
+                __builtin_amdgcn_wave_barrier();
+            }
+        }
+    } else {
+        // 16-bit staging.  After conversion, lane pairs (l, l+32) exchange
+        // halves with v_permlane32_swap so each lane holds eight consecutive
+        // columns (16 bytes): lane l gets columns 16c + 8(l/32) + 0..7, c = 0, 1,
+        // of each 32-column tile.  Reads give 8 lanes per 128-byte row
+        // segment; the two rows of a 16-lane group are 8 apart (bank-disjoint).
+        constexpr bool kBf = MODE != EPI_GELU;
+        unsigned short* const st = reinterpret_cast<unsigned short*>(region);
+        const int ch = lane & 7, rs = lane >> 3;
+        const int col = wcol0 + ch * 8;
+#pragma unroll
+        for (int i = 0; i < kTM; ++i) {
+#pragma unroll
+            for (int j = 0; j < kTN; ++j) {
+                unsigned pk[4][2];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    float v[4];
+                    v[0] = fmaf(acc[j][i][4 * q + 0], sc, bq[j][q].x);
+                    v[1] = fmaf(acc[j][i][4 * q + 1], sc, bq[j][q].y);
+                    v[2] = fmaf(acc[j][i][4 * q + 2], sc, bq[j][q].z);
+                    v[3] = fmaf(acc[j][i][4 * q + 3], sc, bq[j][q].w);
+                    if constexpr (MODE == EPI_GELU) {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) v[r] = gelu_fast(v[r]);
+                    } else {
+                        // EPI_STORE: columns < scale_cols scaled; EPI_QKV_CACHE:
+                        // the query columns (< d_model) scaled
+                        const int c4 = wcol0 + j * 32 + 8 * q + 4 * lhalf;
+                        const int lim = MODE == EPI_STORE ? epi.scale_cols : epi.d_model;
+                        const float cs = c4 < lim ? epi.col_scale : 1.0f;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) v[r] = v[r] * cs;
+                    }
+                    pk[q][0] = pack2<kBf>(v[0], v[1]);
+                    pk[q][1] = pack2<kBf>(v[2], v[3]);
+                }
+#pragma unroll
+                for (int c = 0; c < 2; ++c) {
+                    u32x4 o;
+#pragma unroll
+                    for (int w = 0; w < 2; ++w) {
+                        const auto r = __builtin_amdgcn_permlane32_swap(pk[2 * c][w], pk[2 * c + 1][w],
+                                                                        false, false);
+                        o[w] = r[0];
+                        o[2 + w] = r[1];
+                    }
+                    *reinterpret_cast<u32x4*>(st + lrow * kStage16 + j * 32 + 16 * c + 8 * lhalf) = o;
+                }
+            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                const int rl = 16 * (p >> 1) + 4 * (p & 1) + (rs >> 1) + 8 * (rs & 1);
+                const u32x4 o = *reinterpret_cast<const u32x4*>(st + rl * kStage16 + ch * 8);
+                const int64_t row = wrow0 + i * 32 + rl;
+                if (row >= M || col >= N) continue;          // N is a multiple of 8
+                unsigned short* dst;
+                if constexpr (MODE == EPI_QKV_CACHE) {
+                    const int d = epi.d_model;
+                    if (col < d) {
+                        dst = static_cast<unsigned short*>(epi.out) + row * epi.ldo + col;
+                    } else {   // 8 columns never straddle a head (head_dim % 8 == 0)
+                        const int part = col >= 2 * d ? 2 : 1;
+                        const int c = col - part * d;
+                        const int h = c / epi.head_dim, e = c - h * epi.head_dim;
+                        unsigned short* plane =
+                            static_cast<unsigned short*>(part == 1 ? epi.cache_k : epi.cache_v);
+                        dst = plane + ((int64_t)h * epi.cache_cap + (epi.row0 + row)) * epi.head_dim + e;
+                    }
+                } else {
+                    dst = static_cast<unsigned short*>(epi.out) + row * epi.ldo + col;
+                }
+                __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(dst));
+            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            __builtin_amdgcn_wave_barrier();
+        }
+    }
 }
 
 template <int MODE>
@@ -229,148 +380,130 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict
     const int wsel = __builtin_amdgcn_readfirstlane(wave) >> 1;
     f16* const sbase = wsel == 0 ? sA0 : wsel == 1 ? sA1 : wsel == 2 ? sB0 : sB1;
     char* const region = reinterpret_cast<char*>(sbase) + (wave & 1) * kRegionBytes;
-    const int64_t wrow0 = m0 + wm * kWM;
-    const int wcol0 = n0 + wn * kWN;
-    float4 bq[kTN][4];
-#pragma unroll
-    for (int j = 0; j < kTN; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int col = wcol0 + j * 32 + 8 * q + 4 * lhalf;
-            bq[j][q] = col < N ? *reinterpret_cast<const float4*>(epi.bias + col)
-                               : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-    const float sc = epi.acc_scale;
-
-    if constexpr (MODE == EPI_RESID) {
-        // fp32 staging: a lane writes its four-column runs (16 bytes); reads
-        // give 16 lanes per 256-byte row segment, 4 rows per instruction.
-        float* const st = reinterpret_cast<float*>(region);
-        const int ch = lane & 15;
-        const int col = wcol0 + ch * 4;
-#pragma unroll
-        for (int i = 0; i < kTM; ++i) {
-#pragma unroll
-            for (int j = 0; j < kTN; ++j)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    float4 v;
-                    v.x = fmaf(acc[j][i][4 * q + 0], sc, bq[j][q].x);
-                    v.y = fmaf(acc[j][i][4 * q + 1], sc, bq[j][q].y);
-                    v.z = fmaf(acc[j][i][4 * q + 2], sc, bq[j][q].z);
-                    v.w = fmaf(acc[j][i][4 * q + 3], sc, bq[j][q].w);
-                    *reinterpret_cast<float4*>(st + lrow * kStage32 + j * 32 + 8 * q + 4 * lhalf) = v;
-                }
-            __builtin_amdgcn_s_waitcnt(0xC07F);
-            __builtin_amdgcn_wave_barrier();
-            float4 x[8], g[8];
-#pragma unroll
-            for (int p = 0; p < 8; ++p) {
-                const int rl = p * 4 + (lane >> 4);
-                const int64_t row = wrow0 + i * 32 + rl;
-                x[p] = *reinterpret_cast<const float4*>(st + rl * kStage32 + ch * 4);
-                if (row < M && col < N)
-                    g[p] = *reinterpret_cast<const float4*>(epi.resid + row * epi.ldr + col);
-            }
-#pragma unroll
-            for (int p = 0; p < 8; ++p) {
-                const int64_t row = wrow0 + i * 32 + p * 4 + (lane >> 4);
-                if (row >= M || col >= N) continue;
-                float4 o = g[p];
-                o.x += x[p].x; o.y += x[p].y; o.z += x[p].z; o.w += x[p].w;
-                __builtin_nontemporal_store(f32x4{o.x, o.y, o.z, o.w}, reinterpret_cast<f32x4*>(epi.resid + row * epi.ldr + col));
-            }
-            __builtin_amdgcn_s_waitcnt(0xC07F);
-            __builtin_amdgcn_wave_barrier();
-        }
-    } else {
-        // 16-bit staging.  After conversion, lane pairs (l, l+32) exchange
-        // halves with v_permlane32_swap so each lane holds eight consecutive
-        // columns (16 bytes): lane l gets columns 16c + 8(l/32) + 0..7, c = 0, 1,
-        // of each 32-column tile.  Reads give 8 lanes per 128-byte row
-        // segment; the two rows of a 16-lane group are 8 apart (bank-disjoint).
-        constexpr bool kBf = MODE != EPI_GELU;
-        unsigned short* const st = reinterpret_cast<unsigned short*>(region);
-        const int ch = lane & 7, rs = lane >> 3;
-        const int col = wcol0 + ch * 8;
-#pragma unroll
-        for (int i = 0; i < kTM; ++i) {
-#pragma unroll
-            for (int j = 0; j < kTN; ++j) {
-                unsigned pk[4][2];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    float v[4];
-                    v[0] = fmaf(acc[j][i][4 * q + 0], sc, bq[j][q].x);
-                    v[1] = fmaf(acc[j][i][4 * q + 1], sc, bq[j][q].y);
-                    v[2] = fmaf(acc[j][i][4 * q + 2], sc, bq[j][q].z);
-                    v[3] = fmaf(acc[j][i][4 * q + 3], sc, bq[j][q].w);
-                    if constexpr (MODE == EPI_GELU) {
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) v[r] = gelu_fast(v[r]);
-                    } else {
-                        // EPI_STORE: columns < scale_cols scaled; EPI_QKV_CACHE:
-                        // the query columns (< d_model) scaled
-                        const int c4 = wcol0 + j * 32 + 8 * q + 4 * lhalf;
-                        const int lim = MODE == EPI_STORE ? epi.scale_cols : epi.d_model;
-                        const float cs = c4 < lim ? epi.col_scale : 1.0f;
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) v[r] = v[r] * cs;
-                    }
-                    pk[q][0] = pack2<kBf>(v[0], v[1]);
-                    pk[q][1] = pack2<kBf>(v[2], v[3]);
-                }
-#pragma unroll
-                for (int c = 0; c < 2; ++c) {
-                    u32x4 o;
-#pragma unroll
-                    for (int w = 0; w < 2; ++w) {
-                        const auto r = __builtin_amdgcn_permlane32_swap(pk[2 * c][w], pk[2 * c + 1][w],
-                                                                        false, false);
-                        o[w] = r[0];
-                        o[2 + w] = r[1];
-                    }
-                    *reinterpret_cast<u32x4*>(st + lrow * kStage16 + j * 32 + 16 * c + 8 * lhalf) = o;
-                }
-            }
-            __builtin_amdgcn_s_waitcnt(0xC07F);
-            __builtin_amdgcn_wave_barrier();
-#pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                const int rl = 16 * (p >> 1) + 4 * (p & 1) + (rs >> 1) + 8 * (rs & 1);
-                const u32x4 o = *reinterpret_cast<const u32x4*>(st + rl * kStage16 + ch * 8);
-                const int64_t row = wrow0 + i * 32 + rl;
-                if (row >= M || col >= N) continue;          // N is a multiple of 8
-                unsigned short* dst;
-                if constexpr (MODE == EPI_QKV_CACHE) {
-                    const int d = epi.d_model;
-                    if (col < d) {
-                        dst = static_cast<unsigned short*>(epi.out) + row * epi.ldo + col;
-                    } else {   // 8 columns never straddle a head (head_dim % 8 == 0)
-                        const int part = col >= 2 * d ? 2 : 1;
-                        const int c = col - part * d;
-                        const int h = c / epi.head_dim, e = c - h * epi.head_dim;
-                        unsigned short* plane =
-                            static_cast<unsigned short*>(part == 1 ? epi.cache_k : epi.cache_v);
-                        dst = plane + ((int64_t)h * epi.cache_cap + (epi.row0 + row)) * epi.head_dim + e;
-                    }
-                } else {
-                    dst = static_cast<unsigned short*>(epi.out) + row * epi.ldo + col;
-                }
-                __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(dst));
-            }
-            __builtin_amdgcn_s_waitcnt(0xC07F);
-            __builtin_amdgcn_wave_barrier();
-        }
-    }
+    store_tile<MODE, 32>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane);
     if (lead) __builtin_amdgcn_s_barrier();
 }
 
+// Two-workgroups-per-CU variant: 256 x 128 tiles, four waves of 128 x 64,
+// K-steps of 32, 48 KB of LDS, so a second workgroup shares the CU and one
+// workgroup's epilogue overlaps the other's MFMAs.
+namespace w2 {
+constexpr int kBN = 128, kBK = 32, kThreads = 256;
+// LDS rows of 64 bytes (32 fp16), four 16-byte chunks XORed with (row/4)%4:
+// the 16 rows of a fragment read then cover all 64 banks.
+__device__ __forceinline__ int swz(int row, int chunk) {
+    return row * kBK + ((chunk ^ ((row >> 2) & 3)) << 3);
+}
+}  // namespace w2
+
+template <int MODE>
+__global__ __launch_bounds__(w2::kThreads, 2) void k_gemm_mfma2(const f16* __restrict__ A, int64_t lda,
+                                                               const f16* __restrict__ W, int64_t M,
+                                                               int N, int K, Epilogue epi) {
+    using namespace w2;
+    __shared__ __attribute__((aligned(16))) f16 sA0[kBM * w2::kBK];
+    __shared__ __attribute__((aligned(16))) f16 sA1[kBM * w2::kBK];
+    __shared__ __attribute__((aligned(16))) f16 sB0[w2::kBN * w2::kBK];
+    __shared__ __attribute__((aligned(16))) f16 sB1[w2::kBN * w2::kBK];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int tiles_n = (N + w2::kBN - 1) / w2::kBN;
+    const int t = xcd_tile(blockIdx.x, gridDim.x);
+    const int64_t m0 = (int64_t)(t / tiles_n) * kBM;
+    const int n0 = (t % tiles_n) * w2::kBN;
+
+    const int64_t rows_a = M - m0 < kBM ? M - m0 : kBM;
+    const int rows_b = N - n0 < w2::kBN ? N - n0 : w2::kBN;
+    const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(A + m0 * lda), (short)0, (int)(rows_a * lda * 2), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(W + (int64_t)n0 * K), (short)0, (int)((int64_t)rows_b * K * 2), 0x00020000);
+
+    // A load instruction fills 16 rows (64 lanes x 16 bytes); load i of wave
+    // w covers rows 16 (w kL + i) + lane/4, whose key (row/4)%4 = (lane/16)%4.
+    constexpr int kLA = kBM * 4 / w2::kThreads, kLB = w2::kBN * 4 / w2::kThreads;   // 4, 2
+    const int lch = (lane & 3) ^ ((lane >> 4) & 3);
+    const int voA = (int)(((wave * kLA) * 16 + (lane >> 2)) * lda * 2 + lch * 16);
+    const int voB = ((wave * kLB) * 16 + (lane >> 2)) * K * 2 + lch * 16;
+    const int rowstepA = (int)(16 * lda * 2), rowstepB = 16 * K * 2;
+    auto issue_loads = [&](f16* dA, f16* dB, int k0) {
+        int rsa = rowstepA, rsb = rowstepB;
+        asm volatile("" : "+s"(rsa), "+s"(rsb));
+#pragma unroll
+        for (int i = 0; i < kLA; ++i)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rsA, (__attribute__((address_space(3))) void*)(dA + (wave * kLA + i) * 64 * 8),
+                16, voA + i * rsa + k0 * 2, 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < kLB; ++i)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rsB, (__attribute__((address_space(3))) void*)(dB + (wave * kLB + i) * 64 * 8),
+                16, voB + i * rsb + k0 * 2, 0, 0, 0);
+    };
+
+    f32x16 acc[kTN][kTM];
+#pragma unroll
+    for (int j = 0; j < kTN; ++j)
+#pragma unroll
+        for (int i = 0; i < kTM; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
+
+    const int lrow = lane & 31, lhalf = lane >> 5;
+    const int nk = K / w2::kBK;
+    auto kstep = [&](const f16* cA, const f16* cB, f16* nA, f16* nB, int t) {
+        if (t + 1 < nk) issue_loads(nA, nB, (t + 1) * w2::kBK);
+        h8 a[2][kTM], b[2][kTN];
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            const int ch = kk * 2 + lhalf;
+#pragma unroll
+            for (int i = 0; i < kTM; ++i)
+                a[kk][i] = *reinterpret_cast<const h8*>(&cA[w2::swz(wm * kWM + i * 32 + lrow, ch)]);
+#pragma unroll
+            for (int j = 0; j < kTN; ++j)
+                b[kk][j] = *reinterpret_cast<const h8*>(&cB[w2::swz(wn * kWN + j * 32 + lrow, ch)]);
+        }
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+            for (int j = 0; j < kTN; ++j)
+#pragma unroll
+                for (int i = 0; i < kTM; ++i)
+                    acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(b[kk][j], a[kk][i],
+                                                                       acc[j][i], 0, 0, 0);
+        __builtin_amdgcn_s_waitcnt(0x0F70);     // vmcnt(0): the next stage has landed
+        __syncthreads();
+    };
+    issue_loads(sA0, sB0, 0);
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __syncthreads();
+    int kt = 0;
+    for (; kt + 2 <= nk; kt += 2) {
+        kstep(sA0, sB0, sA1, sB1, kt);
+        kstep(sA1, sB1, sA0, sB0, kt + 1);
+    }
+    if (kt < nk) kstep(sA0, sB0, sA1, sB1, kt);
+
+    // epilogue: regions of 8 KB in the A stages (all reads have finished)
+    char* const region = reinterpret_cast<char*>(wave < 2 ? sA0 : sA1) + (wave & 1) * 8192;
+    store_tile<MODE, 16>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane);
+}
+
+#ifndef GEMM_TWO_PER_CU
+#define GEMM_TWO_PER_CU 0
+#endif
 template <int MODE>
 hipError_t launch_mode(const f16* A, int64_t lda, const f16* W, int64_t M, int N, int K,
                        const Epilogue& epi, hipStream_t s) {
-    const int64_t tiles = ((M + kBM - 1) / kBM) * (int64_t)((N + kBN - 1) / kBN);
-    k_gemm_mfma<MODE><<<(unsigned)tiles, kThreads, 0, s>>>(A, lda, W, M, N, K, epi);
+    if (GEMM_TWO_PER_CU) {
+        const int64_t tiles = ((M + kBM - 1) / kBM) * (int64_t)((N + w2::kBN - 1) / w2::kBN);
+        k_gemm_mfma2<MODE><<<(unsigned)tiles, w2::kThreads, 0, s>>>(A, lda, W, M, N, K, epi);
+    } else {
+        const int64_t tiles = ((M + kBM - 1) / kBM) * (int64_t)((N + kBN - 1) / kBN);
+        k_gemm_mfma<MODE><<<(unsigned)tiles, kThreads, 0, s>>>(A, lda, W, M, N, K, epi);
+    }
     return hipGetLastError();
 }
 

@@ -98,7 +98,8 @@ __device__ __forceinline__ unsigned pack2(float a, float b) {
 // register r of tile (j, i) holds row 32i + lane%32 and column
 // 32j + 8(r/4) + 4(lane/32) + r%4 of the wave tile at (wrow0, wcol0)),
 // staged through the wave's own LDS region (fp32 residual passes of RROWS
-// rows: RROWS x 272 bytes; 16-bit passes of 32 rows: 32 x 144 bytes).
+// rows: RROWS x 272 bytes; 16-bit passes of 32 rows: 32 x 144 bytes; the
+// region must hold the larger).
 template <int MODE, int RROWS>
 __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* const region,
                                            int64_t wrow0, int wcol0, int64_t M, int N,
@@ -384,126 +385,11 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict
     if (lead) __builtin_amdgcn_s_barrier();
 }
 
-// Two-workgroups-per-CU variant: 256 x 128 tiles, four waves of 128 x 64,
-// K-steps of 32, 48 KB of LDS, so a second workgroup shares the CU and one
-// workgroup's epilogue overlaps the other's MFMAs.
-namespace w2 {
-constexpr int kBN = 128, kBK = 32, kThreads = 256;
-// LDS rows of 64 bytes (32 fp16), four 16-byte chunks XORed with (row/4)%4:
-// the 16 rows of a fragment read then cover all 64 banks.
-__device__ __forceinline__ int swz(int row, int chunk) {
-    return row * kBK + ((chunk ^ ((row >> 2) & 3)) << 3);
-}
-}  // namespace w2
-
-template <int MODE>
-__global__ __launch_bounds__(w2::kThreads, 2) void k_gemm_mfma2(const f16* __restrict__ A, int64_t lda,
-                                                               const f16* __restrict__ W, int64_t M,
-                                                               int N, int K, Epilogue epi) {
-    using namespace w2;
-    __shared__ __attribute__((aligned(16))) f16 sA0[kBM * w2::kBK];
-    __shared__ __attribute__((aligned(16))) f16 sA1[kBM * w2::kBK];
-    __shared__ __attribute__((aligned(16))) f16 sB0[w2::kBN * w2::kBK];
-    __shared__ __attribute__((aligned(16))) f16 sB1[w2::kBN * w2::kBK];
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    const int tiles_n = (N + w2::kBN - 1) / w2::kBN;
-    const int t = xcd_tile(blockIdx.x, gridDim.x);
-    const int64_t m0 = (int64_t)(t / tiles_n) * kBM;
-    const int n0 = (t % tiles_n) * w2::kBN;
-
-    const int64_t rows_a = M - m0 < kBM ? M - m0 : kBM;
-    const int rows_b = N - n0 < w2::kBN ? N - n0 : w2::kBN;
-    const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(A + m0 * lda), (short)0, (int)(rows_a * lda * 2), 0x00020000);
-    const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(W + (int64_t)n0 * K), (short)0, (int)((int64_t)rows_b * K * 2), 0x00020000);
-
-    // A load instruction fills 16 rows (64 lanes x 16 bytes); load i of wave
-    // w covers rows 16 (w kL + i) + lane/4, whose key (row/4)%4 = (lane/16)%4.
-    constexpr int kLA = kBM * 4 / w2::kThreads, kLB = w2::kBN * 4 / w2::kThreads;   // 4, 2
-    const int lch = (lane & 3) ^ ((lane >> 4) & 3);
-    const int voA = (int)(((wave * kLA) * 16 + (lane >> 2)) * lda * 2 + lch * 16);
-    const int voB = ((wave * kLB) * 16 + (lane >> 2)) * K * 2 + lch * 16;
-    const int rowstepA = (int)(16 * lda * 2), rowstepB = 16 * K * 2;
-    auto issue_loads = [&](f16* dA, f16* dB, int k0) {
-        int rsa = rowstepA, rsb = rowstepB;
-        asm volatile("" : "+s"(rsa), "+s"(rsb));
-#pragma unroll
-        for (int i = 0; i < kLA; ++i)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rsA, (__attribute__((address_space(3))) void*)(dA + (wave * kLA + i) * 64 * 8),
-                16, voA + i * rsa + k0 * 2, 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < kLB; ++i)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rsB, (__attribute__((address_space(3))) void*)(dB + (wave * kLB + i) * 64 * 8),
-                16, voB + i * rsb + k0 * 2, 0, 0, 0);
-    };
-
-    f32x16 acc[kTN][kTM];
-#pragma unroll
-    for (int j = 0; j < kTN; ++j)
-#pragma unroll
-        for (int i = 0; i < kTM; ++i)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
-
-    const int lrow = lane & 31, lhalf = lane >> 5;
-    const int nk = K / w2::kBK;
-    auto kstep = [&](const f16* cA, const f16* cB, f16* nA, f16* nB, int t) {
-        if (t + 1 < nk) issue_loads(nA, nB, (t + 1) * w2::kBK);
-        h8 a[2][kTM], b[2][kTN];
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-            const int ch = kk * 2 + lhalf;
-#pragma unroll
-            for (int i = 0; i < kTM; ++i)
-                a[kk][i] = *reinterpret_cast<const h8*>(&cA[w2::swz(wm * kWM + i * 32 + lrow, ch)]);
-#pragma unroll
-            for (int j = 0; j < kTN; ++j)
-                b[kk][j] = *reinterpret_cast<const h8*>(&cB[w2::swz(wn * kWN + j * 32 + lrow, ch)]);
-        }
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-            for (int j = 0; j < kTN; ++j)
-#pragma unroll
-                for (int i = 0; i < kTM; ++i)
-                    acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(b[kk][j], a[kk][i],
-                                                                       acc[j][i], 0, 0, 0);
-        __builtin_amdgcn_s_waitcnt(0x0F70);     // vmcnt(0): the next stage has landed
-        __syncthreads();
-    };
-    issue_loads(sA0, sB0, 0);
-    __builtin_amdgcn_s_waitcnt(0x0F70);
-    __syncthreads();
-    int kt = 0;
-    for (; kt + 2 <= nk; kt += 2) {
-        kstep(sA0, sB0, sA1, sB1, kt);
-        kstep(sA1, sB1, sA0, sB0, kt + 1);
-    }
-    if (kt < nk) kstep(sA0, sB0, sA1, sB1, kt);
-
-    // epilogue: regions of 8 KB in the A stages (all reads have finished)
-    char* const region = reinterpret_cast<char*>(wave < 2 ? sA0 : sA1) + (wave & 1) * 8192;
-    store_tile<MODE, 16>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane);
-}
-
-#ifndef GEMM_TWO_PER_CU
-#define GEMM_TWO_PER_CU 0
-#endif
 template <int MODE>
 hipError_t launch_mode(const f16* A, int64_t lda, const f16* W, int64_t M, int N, int K,
                        const Epilogue& epi, hipStream_t s) {
-    if (GEMM_TWO_PER_CU) {
-        const int64_t tiles = ((M + kBM - 1) / kBM) * (int64_t)((N + w2::kBN - 1) / w2::kBN);
-        k_gemm_mfma2<MODE><<<(unsigned)tiles, w2::kThreads, 0, s>>>(A, lda, W, M, N, K, epi);
-    } else {
-        const int64_t tiles = ((M + kBM - 1) / kBM) * (int64_t)((N + kBN - 1) / kBN);
-        k_gemm_mfma<MODE><<<(unsigned)tiles, kThreads, 0, s>>>(A, lda, W, M, N, K, epi);
-    }
+    const int64_t tiles = ((M + kBM - 1) / kBM) * (int64_t)((N + kBN - 1) / kBN);
+    k_gemm_mfma<MODE><<<(unsigned)tiles, kThreads, 0, s>>>(A, lda, W, M, N, K, epi);
     return hipGetLastError();
 }
 

@@ -218,20 +218,21 @@ def encode(blob, d, H, L, F, hist_emb, hist_offsets, capacity_rows=None, users=N
     return cache
 
 
-def rank(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
-         users=None, cand_rows=None):
-    """Candidate scoring against the cached history (Sec. 3, serving design and
-    KV-cache sharing): only candidate tokens are processed.
+def rank_hidden(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
+                users=None, cand_rows=None):
+    """Candidate forward pass against the cached history (Sec. 3, serving
+    design and KV-cache sharing): only candidate tokens are processed.
 
     For candidate c of user u and every layer: a = LN1(g); q, k_c, v_c from a;
     per head, the logits are q . K_t / sqrt(D) over the user's cached history
     keys t plus q . k_c / sqrt(D) for the candidate's own key; the softmax of
     those n_u + 1 logits weights the cached values plus v_c; then
-    g += O-projection and g += FFN(g).  The score is w . LN_f(g) + b.
+    g += O-projection and g += FFN(g).
 
-    Returns float64 scores for every packed candidate row (NaN for rows not
-    requested).  ``users`` and ``cand_rows`` (absolute packed row indices)
-    restrict the work; candidates are independent, so a subset is exact.
+    Returns the float64 final hidden states g [rows, d] of every packed
+    candidate row (NaN for rows not requested).  ``users`` and ``cand_rows``
+    (absolute packed row indices) restrict the work; candidates are
+    independent, so a subset is exact.
     """
     layers, final = unpack_weights(blob, d, L, F)
     D = d // H
@@ -240,7 +241,7 @@ def rank(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
     C = np.asarray(cand_emb, dtype=np.float64)
     cache = np.asarray(cache, dtype=np.float64)
     U = len(coffs) - 1
-    scores = np.full(C.shape[0], np.nan)
+    hidden = np.full((C.shape[0], d), np.nan)
     wanted = None if cand_rows is None else np.asarray(cand_rows, dtype=np.int64)
     for u in (range(U) if users is None else users):
         rows = np.arange(coffs[u], coffs[u + 1])
@@ -269,7 +270,20 @@ def rank(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
                 o[j] = p[:, :-1] @ Vh + p[:, -1:] * vs[j]
             g = g + linear(o.transpose(1, 0, 2).reshape(kc_rows, d), lw["Wo"], lw["bo"])
             g = g + ffn(g, lw)
-        scores[rows] = score_head(g, final)
+        hidden[rows] = g
+    return hidden
+
+
+def rank(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
+         users=None, cand_rows=None):
+    """Candidate scores w . LN_f(g) + b of the final hidden states
+    (``rank_hidden``); float64, NaN for rows not requested."""
+    _, final = unpack_weights(blob, d, L, F)
+    g = rank_hidden(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
+                    users=users, cand_rows=cand_rows)
+    scores = np.full(g.shape[0], np.nan)
+    ok = ~np.isnan(g[:, 0]) if g.shape[0] else np.zeros(0, dtype=bool)
+    scores[ok] = score_head(g[ok], final)
     return scores
 
 

@@ -193,3 +193,45 @@ def workload_shape(name: str) -> dict:
         spec["n_list"] = np.full(spec["U"], spec["n"])
         spec["k_list"] = np.full(spec["U"], spec["k"])
     return spec
+
+
+# ----------------------------------------------------------------------------
+# Per-action ranking heads (inputs only)
+# ----------------------------------------------------------------------------
+
+# Default action set of the heads workloads: C = 3 action types (for example
+# save, click, hide) with utility weights that reward the first two and
+# penalise the third; hidden width d/2.
+DEFAULT_UTILITY = (1.0, 0.5, -2.0)
+
+
+def heads_layout(d: int, C: int, Fh: int):
+    """Entries of the heads blob in order: per head W1 [Fh, d], b1 [Fh],
+    w2 [1, Fh] (stored flat), b2 [1]."""
+    ent = []
+    for c in range(C):
+        p = f"h{c}."
+        ent += [(p + "W1", (Fh, d), "mat"), (p + "b1", (Fh,), "vec"),
+                (p + "w2", (1, Fh), "mat"), (p + "b2", (1,), "vec")]
+    return ent
+
+
+def make_heads(d: int, C: int = 3, Fh: int = None, dtype: str = "bf16", seed: int = 0,
+               variant: str = "perturbed") -> np.ndarray:
+    """Draw a heads blob (float32; bf16-rounded for bf16 models): Xavier-uniform
+    matrices; biases 0 for ``base``, uniform +-0.1 otherwise."""
+    Fh = d // 2 if Fh is None else Fh
+    rng = np.random.default_rng(seed + 7919)
+    parts = []
+    for _, shape, kind in heads_layout(d, C, Fh):
+        if kind == "mat":
+            fan_out, fan_in = shape
+            a = math.sqrt(6.0 / (fan_in + fan_out))
+            w = rng.uniform(-a, a, size=shape)
+        elif variant == "base":
+            w = np.zeros(shape)
+        else:
+            w = rng.uniform(-0.1, 0.1, size=shape)
+        parts.append(np.asarray(w, dtype=np.float64).reshape(-1))
+    blob = np.concatenate(parts).astype(np.float32)
+    return round_bf16(blob) if dtype == "bf16" else blob

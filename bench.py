@@ -114,6 +114,55 @@ def cpu_baseline(inp, budget_s=12.0):
                       f"{inp.U} users ({cands} candidates), {t_rank:.1f} s"}
 
 
+def actions_topk(args, inp, model, kv, hs, cs, C, Kc, ev, stream):
+    """The serving step after scoring (paper Sec. 3, L0 + L1 deployment): the
+    same forward pass with C = 3 per-action heads (hidden d/2), sigmoid
+    probabilities, utility, and each user's top 1000 by utility.  One step =
+    one upr_rank_actions over every candidate + one upr_topk_by_utility."""
+    import torch
+    from paper_2606_00422_amd import upr
+    from synth import DEFAULT_UTILITY, make_heads
+    n_act, hidden, K = len(DEFAULT_UTILITY), inp.d // 2, 1000
+    heads = upr.Heads(model, n_act, hidden, make_heads(inp.d, n_act, hidden, dtype=inp.dtype,
+                                                       seed=args.seed))
+    U = inp.U
+    probs = torch.empty((max(Kc, 1), n_act), dtype=torch.float32, device="cuda")
+    util = torch.empty(max(Kc, 1), dtype=torch.float32, device="cuda")
+    rows = torch.empty((max(U, 1), K), dtype=torch.int32, device="cuda")
+    vals = torch.empty((max(U, 1), K), dtype=torch.float32, device="cuda")
+    ws = model.workspace(upr.upr_rank_actions_workspace_bytes(model.handle, heads.handle, hs, cs))
+    uw = np.asarray(DEFAULT_UTILITY, dtype=np.float32)
+
+    def step():
+        upr.upr_rank_actions(model.handle, heads.handle, kv, hs, C.data_ptr(), cs, uw,
+                             probs.data_ptr(), util.data_ptr(), ws.data_ptr(), ws.numel(), stream)
+        upr.upr_topk_by_utility(util.data_ptr(), cs, K, rows.data_ptr(), vals.data_ptr(), stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = ev(), ev()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    assert bool(torch.isfinite(probs[:Kc]).all()), "non-finite action probabilities"
+    upr.upr_profile_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    prof = upr.upr_profile_read()
+    upr.upr_profile_enable(False)
+    heads.close()
+    extra = {k: round(v[1] / v[0], 5) for k, v in prof.items()
+             if k in ("rank.lnf", "rank.heads_hidden", "rank.heads_out", "topk")}
+    return {"ms_per_step": round(ms, 4), "candidates_per_s": round(Kc / (ms * 1e-3), 1),
+            "n_actions": n_act, "head_hidden": hidden, "K": K,
+            "utility_weights": list(DEFAULT_UTILITY), "extra_kernels_avg_ms": extra}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -123,6 +172,8 @@ def main():
     ap.add_argument("--user-reps", type=int, default=3, help="reps of the per-user latency pass")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-actions", action="store_true",
+                    help="skip the per-action heads + utility top-K measurement")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this path has no "
@@ -256,6 +307,8 @@ def main():
         "roofline": roof,
         "kernels": kernels,
     }
+    if not args.no_actions:
+        out["actions_topk"] = actions_topk(args, inp, model, kv, hs, cs, C, Kc, ev, stream)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(inp)
     print(json.dumps(out), flush=True)

@@ -49,7 +49,8 @@ typedef enum {
     UPR_ERR_WORKSPACE = 5,  /* workspace too small or misaligned               */
     UPR_ERR_DTYPE = 6,      /* unknown arithmetic type                         */
     UPR_ERR_HIP = 7,        /* a HIP runtime call failed                       */
-    UPR_ERR_WEIGHTS = 8     /* weight blob has the wrong number of values      */
+    UPR_ERR_WEIGHTS = 8,    /* weight blob has the wrong number of values      */
+    UPR_ERR_LIMIT = 9       /* an argument exceeds a documented limit          */
 } upr_status;
 
 typedef enum { UPR_F32 = 0, UPR_BF16 = 1 } upr_dtype;
@@ -163,6 +164,77 @@ upr_status upr_rank_candidates(const upr_model* model, const upr_kv_cache* cache
                                const upr_segments* hist, const void* cand_emb,
                                const upr_segments* cand, float* scores,
                                void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------
+ * Per-action ranking heads and utility top-K (paper Sec. 3: the ranking
+ * objective of Masked Action Modeling gives every action type c = 1..C its
+ * own MLP head h_psi_c producing a scalar logit from the transformer's
+ * hidden state; the unified L0 + L1 service returns the top K candidates by
+ * the heads' utility functions).
+ * Readings of the paper fixed here: each head reads z = LayerNorm_f(h) (the
+ * model's final LayerNorm, the input of the single score head), has one
+ * hidden layer of width `hidden` with tanh-form GELU,
+ *   logit_c = w2_c . GELU(W1_c z + b1_c) + b2_c,   p_c = sigmoid(logit_c),
+ * and the utility of a candidate is sum_c u_c p_c with caller-given u_c.
+ * --------------------------------------------------------------------- */
+typedef struct upr_heads upr_heads;     /* opaque */
+
+/* C action heads of width `hidden`.  Supported: 1 <= n_actions <= 8,
+ * hidden >= 8, n_actions * hidden a multiple of 8 and at most 8192. */
+typedef struct {
+    int32_t n_actions;
+    int32_t hidden;
+} upr_heads_config;
+
+/* Number of float values in a heads blob (-1 if cfg or hc is invalid).
+ * Blob order (float32), per head c: W1[hidden, d_model] ([out, in]),
+ * b1[hidden], w2[hidden], b2[1]. */
+int64_t upr_heads_weights_count(const upr_config* cfg, const upr_heads_config* hc);
+
+/* Create heads for `model` (same device; rounding and storage as the model's
+ * weights: bf16 models round every value to bf16 and keep the stacked W1 as
+ * fp16 after an exact power-of-two scaling).  Allocates device memory.
+ * *out is set only on UPR_OK. */
+upr_status upr_heads_create(const upr_model* model, const upr_heads_config* hc,
+                            const float* weights_host, int64_t weights_count,
+                            upr_heads** out);
+
+/* Release heads (NULL is ignored).  No call may be using them. */
+void upr_heads_destroy(upr_heads* heads);
+
+/* Workspace bytes needed by upr_rank_actions (0 on invalid input). */
+size_t upr_rank_actions_workspace_bytes(const upr_model* model, const upr_heads* heads,
+                                        const upr_segments* hist, const upr_segments* cand);
+
+/* Candidate ranking with the per-action heads: the same forward pass as
+ * upr_rank_candidates, then the C heads on LayerNorm_f of each candidate's
+ * final hidden state.
+ * utility_weights: host float32 [n_actions], the u_c (read during the call).
+ * probs: device float32 [rows, n_actions] row-major, indexed like cand_emb
+ * rows, receives p_c; may be NULL.  utility: device float32 [rows], indexed
+ * like cand_emb rows, receives sum_c u_c p_c; may be NULL (not both NULL).
+ * Other arguments as for upr_rank_candidates. */
+upr_status upr_rank_actions(const upr_model* model, const upr_heads* heads,
+                            const upr_kv_cache* cache, const upr_segments* hist,
+                            const void* cand_emb, const upr_segments* cand,
+                            const float* utility_weights, float* probs, float* utility,
+                            void* ws, size_t ws_bytes, void* stream);
+
+/* Largest candidate count of one user that upr_topk_by_utility accepts. */
+#define UPR_TOPK_MAX_CANDIDATES 16384
+
+/* Per-user top K by utility (paper Sec. 3, deployment configurations).
+ * utility: device float32, indexed like the candidate rows of `cand` (for
+ * example the output of upr_rank_actions).  For each user u, writes row u of
+ * topk_rows (device int32 [num_users, K]): the absolute candidate rows of its
+ * K highest utilities, highest first; equal utilities keep the lower row
+ * first; NaN utilities come after every number; -1 pads rows past the
+ * user's candidate count.  topk_utility (device float32 [num_users, K], may
+ * be NULL) receives the matching utilities (NaN in padding).  Requires
+ * K >= 1 and at most UPR_TOPK_MAX_CANDIDATES candidates per user
+ * (UPR_ERR_LIMIT otherwise).  Allocates nothing. */
+upr_status upr_topk_by_utility(const float* utility, const upr_segments* cand, int32_t K,
+                               int32_t* topk_rows, float* topk_utility, void* stream);
 
 /* Diagnostics: per-kernel timing with HIP events.  While enabled, encode and
  * rank record a pair of hipEvents on the call's stream around every kernel

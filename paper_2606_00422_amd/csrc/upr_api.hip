@@ -23,6 +23,19 @@ struct upr_model {
     upr::FinalWeights fin;
 };
 
+// Per-action heads: stacked first layers W1 [C*Fh, d] (model matrix type,
+// scaled by 2^k for bf16 models: s_w1 = 2^-k), b1 [C*Fh], w2 [C*Fh], b2 [C].
+struct upr_heads {
+    upr_config cfg;             // of the model the heads were made for
+    int32_t C = 0, Fh = 0;
+    void* dev = nullptr;
+    const void* W1 = nullptr;
+    float s_w1 = 1.0f;
+    const float* b1 = nullptr;
+    const float* w2 = nullptr;
+    const float* b2 = nullptr;
+};
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -100,6 +113,63 @@ upr_status check_segments(const upr_segments* s, const char* name, int64_t* firs
     *last = o[s->num_users];
     return UPR_OK;
 }
+
+// Device image under construction: pieces start on 256-byte boundaries.
+// Matrices: fp32 models copy them; bf16 models round each value to bf16
+// (nearest, ties to even), multiply by an exact power of two 2^k that puts
+// the largest magnitude in [2^14, 2^15), and store fp16 -- exact for every
+// value within 2^29 of that maximum.  *scale receives 2^-k.  Vectors stay
+// fp32.
+struct ImageBuilder {
+    std::vector<char> img;
+    upr_dtype dtype;
+    static size_t align(size_t x) { return (x + 255) & ~size_t(255); }
+    size_t add_mat(const float* src, int64_t n, float* scale) {
+        const size_t es = dtype == UPR_BF16 ? 2 : 4;
+        size_t off = align(img.size());
+        img.resize(off + n * es);
+        *scale = 1.0f;
+        if (dtype == UPR_BF16) {
+            float maxabs = 0.f;
+            for (int64_t i = 0; i < n; ++i)
+                maxabs = std::fmax(maxabs, std::fabs(bf16_value(f32_to_bf16_rne(src[i]))));
+            int k = 0;
+            if (maxabs > 0.f && std::isfinite(maxabs)) {
+                int ex;
+                std::frexp(maxabs, &ex);               // maxabs in [2^(ex-1), 2^ex)
+                k = std::min(100, std::max(-100, 15 - ex));
+            }
+            const float up = std::ldexp(1.0f, k);
+            *scale = std::ldexp(1.0f, -k);
+            _Float16* dst = reinterpret_cast<_Float16*>(img.data() + off);
+            for (int64_t i = 0; i < n; ++i)
+                dst[i] = (_Float16)(bf16_value(f32_to_bf16_rne(src[i])) * up);
+        } else {
+            std::memcpy(img.data() + off, src, n * 4);
+        }
+        return off;
+    }
+    size_t add_vec(const float* src, int64_t n) {
+        size_t off = align(img.size());
+        img.resize(off + n * 4);
+        std::memcpy(img.data() + off, src, n * 4);
+        return off;
+    }
+    // Copies the image to new device memory (*dev) or fails.
+    upr_status upload(void** dev) {
+        img.resize(align(img.size()));
+        hipError_t e = hipMalloc(dev, img.size());
+        if (e != hipSuccess)
+            return fail(UPR_ERR_HIP, "hipMalloc(%zu) failed: %s", img.size(), hipGetErrorString(e));
+        e = hipMemcpy(*dev, img.data(), img.size(), hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            (void)hipFree(*dev);
+            *dev = nullptr;
+            return fail(UPR_ERR_HIP, "hipMemcpy of weights failed: %s", hipGetErrorString(e));
+        }
+        return UPR_OK;
+    }
+};
 
 upr_status check_workspace(void* ws, size_t ws_bytes, size_t need) {
     if (need == 0) return UPR_OK;
@@ -258,11 +328,21 @@ static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_
     return UPR_OK;
 }
 
+// Outputs of a rank pass: the single score, or the action heads'
+// probabilities / utilities.
+struct RankOut {
+    float* scores = nullptr;
+    const upr_heads* heads = nullptr;
+    HeadUtility uw{};
+    float* probs = nullptr;
+    float* util = nullptr;
+};
+
 template <typename Types>
 static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
                            const upr_segments* hist, const typename Types::kv* cand_emb,
-                           const upr_segments* cand, float* scores, const RankPlan& p, char* ws,
-                           hipStream_t s) {
+                           const upr_segments* cand, const RankOut& out, const RankPlan& p,
+                           char* ws, hipStream_t s) {
     using T = typename Types::kv;
     using TA = typename Types::act;
     const upr_config& c = m->cfg;
@@ -313,7 +393,28 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
                                                cache->capacity_rows, s));
         UPR_HIP(launch_ffn_block<Types>(kRankFfnNames, w, o, a, h, g, R, d, F, c.ln_eps, s));
     }
-    UPR_LAUNCH("rank.score_head", launch_score_head(g, scores + p.row0, R, d, m->fin, c.ln_eps, s));
+    if (!out.heads) {
+        UPR_LAUNCH("rank.score_head",
+                   launch_score_head(g, out.scores + p.row0, R, d, m->fin, c.ln_eps, s));
+        return UPR_OK;
+    }
+    // action heads: z = LN_f(g); hid = gelu(z W1^T + b1) (all heads stacked);
+    // per head logit, sigmoid, utility
+    const upr_heads* hd = out.heads;
+    const int HC = hd->C * hd->Fh;
+    UPR_LAUNCH("rank.lnf", launch_layernorm<TA>(g, a, R, d, m->fin.lnf_g, m->fin.lnf_b, c.ln_eps, s));
+    Epilogue e{};
+    e.mode = EPI_GELU;
+    e.acc_scale = hd->s_w1;
+    e.bias = hd->b1;
+    e.out = h;
+    e.ldo = HC;
+    UPR_LAUNCH("rank.heads_hidden",
+               launch_gemm<TA, T>(a, d, static_cast<const TA*>(hd->W1), R, HC, d, e, s));
+    UPR_LAUNCH("rank.heads_out",
+               launch_heads_out<TA>(h, HC, R, hd->C, hd->Fh, hd->w2, hd->b2, out.uw,
+                                    out.probs ? out.probs + p.row0 * hd->C : nullptr,
+                                    out.util ? out.util + p.row0 : nullptr, s));
     return UPR_OK;
 }
 
@@ -340,45 +441,11 @@ upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
         return fail(UPR_ERR_WEIGHTS, "weight blob has %lld values, config needs %lld",
                     (long long)count, (long long)weights_count(c));
     const int64_t d = c.d_model, F = c.d_ff;
-    const size_t es = elem_size(c);
     // Device image: per layer the four matrices (model dtype), then all
-    // vectors (fp32).  Every piece starts on a 256-byte boundary.
-    std::vector<char> img;
-    auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
-    // Matrices: fp32 models copy them; bf16 models round each value to bf16
-    // (nearest, ties to even), multiply by an exact power of two 2^k that puts
-    // the largest magnitude in [2^14, 2^15), and store fp16 -- exact for every
-    // value within 2^29 of that maximum.  *scale receives 2^-k.
-    auto add_mat = [&](const float* src, int64_t n, float* scale) {
-        size_t off = align(img.size());
-        img.resize(off + n * es);
-        *scale = 1.0f;
-        if (c.dtype == UPR_BF16) {
-            float maxabs = 0.f;
-            for (int64_t i = 0; i < n; ++i)
-                maxabs = std::fmax(maxabs, std::fabs(bf16_value(f32_to_bf16_rne(src[i]))));
-            int k = 0;
-            if (maxabs > 0.f && std::isfinite(maxabs)) {
-                int ex;
-                std::frexp(maxabs, &ex);               // maxabs in [2^(ex-1), 2^ex)
-                k = std::min(100, std::max(-100, 15 - ex));
-            }
-            const float up = std::ldexp(1.0f, k);
-            *scale = std::ldexp(1.0f, -k);
-            _Float16* dst = reinterpret_cast<_Float16*>(img.data() + off);
-            for (int64_t i = 0; i < n; ++i)
-                dst[i] = (_Float16)(bf16_value(f32_to_bf16_rne(src[i])) * up);
-        } else {
-            std::memcpy(img.data() + off, src, n * 4);
-        }
-        return off;
-    };
-    auto add_vec = [&](const float* src, int64_t n) {
-        size_t off = align(img.size());
-        img.resize(off + n * 4);
-        std::memcpy(img.data() + off, src, n * 4);
-        return off;
-    };
+    // vectors (fp32).
+    ImageBuilder ib{{}, (upr_dtype)c.dtype};
+    auto add_mat = [&](const float* src, int64_t n, float* scale) { return ib.add_mat(src, n, scale); };
+    auto add_vec = [&](const float* src, int64_t n) { return ib.add_vec(src, n); };
     struct LayerOff {
         size_t Wqkv, Wo, W1, W2, ln1_g, ln1_b, bqkv, bo, ln2_g, ln2_b, b1, b2;
         float s_qkv, s_o, s_1, s_2;
@@ -426,22 +493,15 @@ upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
     const size_t off_lnf_b = add_vec(p, d); p += d;
     const size_t off_ws = add_vec(p, d); p += d;
     const size_t off_bs = add_vec(p, 1); p += 1;
-    img.resize(align(img.size()));
 
     upr_model* m = new upr_model();
     m->cfg = c;
-    m->dev_bytes = img.size();
-    hipError_t e = hipMalloc(&m->dev, m->dev_bytes);
-    if (e != hipSuccess) {
+    st = ib.upload(&m->dev);
+    if (st != UPR_OK) {
         delete m;
-        return fail(UPR_ERR_HIP, "hipMalloc(%zu) failed: %s", img.size(), hipGetErrorString(e));
+        return st;
     }
-    e = hipMemcpy(m->dev, img.data(), img.size(), hipMemcpyHostToDevice);
-    if (e != hipSuccess) {
-        (void)hipFree(m->dev);
-        delete m;
-        return fail(UPR_ERR_HIP, "hipMemcpy of weights failed: %s", hipGetErrorString(e));
-    }
+    m->dev_bytes = ib.img.size();
     char* base = static_cast<char*>(m->dev);
     auto fp = [&](size_t off) { return reinterpret_cast<const float*>(base + off); };
     for (int l = 0; l < c.n_layers; ++l) {
@@ -563,12 +623,168 @@ upr_status upr_rank_candidates(const upr_model* m, const upr_kv_cache* cache,
     if (p.rows == 0) return ok();
     hipStream_t s = static_cast<hipStream_t>(stream);
     char* w = static_cast<char*>(ws);
+    upr::RankOut out;
+    out.scores = scores;
     st = m->cfg.dtype == UPR_BF16
              ? upr::run_rank<upr::Bf16Types>(m, cache, hist, static_cast<const bf16*>(cand_emb),
-                                             cand, scores, p, w, s)
+                                             cand, out, p, w, s)
              : upr::run_rank<upr::F32Types>(m, cache, hist, static_cast<const float*>(cand_emb),
-                                            cand, scores, p, w, s);
+                                            cand, out, p, w, s);
     return st == UPR_OK ? ok() : st;
+}
+
+// ---- per-action heads and utility top-K
+
+static upr_status check_heads_config(const upr_config* cfg, const upr_heads_config* hc) {
+    upr_status st = check_config(cfg);
+    if (st != UPR_OK) return st;
+    if (!hc) return fail(UPR_ERR_NULL, "heads config is NULL");
+    if (hc->n_actions < 1 || hc->n_actions > upr::kMaxActions)
+        return fail(UPR_ERR_CONFIG, "n_actions %d outside [1, %d]", hc->n_actions, upr::kMaxActions);
+    if (hc->hidden < 8 || hc->hidden % 8 != 0 || (int64_t)hc->n_actions * hc->hidden > 8192)
+        return fail(UPR_ERR_CONFIG, "hidden %d must be a multiple of 8, >= 8, with n_actions * hidden <= 8192",
+                    hc->hidden);
+    return UPR_OK;
+}
+
+int64_t upr_heads_weights_count(const upr_config* cfg, const upr_heads_config* hc) {
+    if (check_heads_config(cfg, hc) != UPR_OK) return -1;
+    return (int64_t)hc->n_actions * ((int64_t)hc->hidden * cfg->d_model + 2 * hc->hidden + 1);
+}
+
+upr_status upr_heads_create(const upr_model* m, const upr_heads_config* hc,
+                            const float* weights_host, int64_t count, upr_heads** out) {
+    if (!m) return fail(UPR_ERR_NULL, "model is NULL");
+    upr_status st = check_heads_config(&m->cfg, hc);
+    if (st != UPR_OK) return st;
+    if (!weights_host) return fail(UPR_ERR_NULL, "weights_host is NULL");
+    if (!out) return fail(UPR_ERR_NULL, "out is NULL");
+    const int64_t need = upr_heads_weights_count(&m->cfg, hc);
+    if (count != need)
+        return fail(UPR_ERR_WEIGHTS, "heads blob has %lld values, config needs %lld",
+                    (long long)count, (long long)need);
+    const int64_t d = m->cfg.d_model, C = hc->n_actions, Fh = hc->hidden;
+    std::vector<float> W1, b1, w2, b2;
+    const float* p = weights_host;
+    for (int64_t c = 0; c < C; ++c) {
+        W1.insert(W1.end(), p, p + Fh * d); p += Fh * d;
+        b1.insert(b1.end(), p, p + Fh); p += Fh;
+        w2.insert(w2.end(), p, p + Fh); p += Fh;
+        b2.push_back(*p); p += 1;
+    }
+    ImageBuilder ib{{}, (upr_dtype)m->cfg.dtype};
+    upr_heads* hd = new upr_heads();
+    const size_t oW1 = ib.add_mat(W1.data(), C * Fh * d, &hd->s_w1);
+    const size_t ob1 = ib.add_vec(b1.data(), C * Fh);
+    const size_t ow2 = ib.add_vec(w2.data(), C * Fh);
+    const size_t ob2 = ib.add_vec(b2.data(), C);
+    st = ib.upload(&hd->dev);
+    if (st != UPR_OK) {
+        delete hd;
+        return st;
+    }
+    char* base = static_cast<char*>(hd->dev);
+    hd->cfg = m->cfg;
+    hd->C = (int32_t)C;
+    hd->Fh = (int32_t)Fh;
+    hd->W1 = base + oW1;
+    hd->b1 = reinterpret_cast<const float*>(base + ob1);
+    hd->w2 = reinterpret_cast<const float*>(base + ow2);
+    hd->b2 = reinterpret_cast<const float*>(base + ob2);
+    *out = hd;
+    return ok();
+}
+
+void upr_heads_destroy(upr_heads* hd) {
+    if (!hd) return;
+    if (hd->dev) (void)hipFree(hd->dev);
+    delete hd;
+}
+
+static bool same_shape(const upr_config& a, const upr_config& b) {
+    return a.d_model == b.d_model && a.n_heads == b.n_heads && a.head_dim == b.head_dim &&
+           a.n_layers == b.n_layers && a.d_ff == b.d_ff && a.dtype == b.dtype;
+}
+
+size_t upr_rank_actions_workspace_bytes(const upr_model* m, const upr_heads* hd,
+                                        const upr_segments* hist, const upr_segments* cand) {
+    if (!m || !hd || !same_shape(m->cfg, hd->cfg)) return 0;
+    int64_t hf, hl, cf, cl;
+    if (check_segments(hist, "hist", &hf, &hl) != UPR_OK) return 0;
+    if (check_segments(cand, "cand", &cf, &cl) != UPR_OK) return 0;
+    if (hist->num_users != cand->num_users) return 0;
+    return upr::plan_rank(m->cfg, cand->num_users, cand->offsets_host, hd->C * hd->Fh).bytes;
+}
+
+upr_status upr_rank_actions(const upr_model* m, const upr_heads* hd, const upr_kv_cache* cache,
+                            const upr_segments* hist, const void* cand_emb,
+                            const upr_segments* cand, const float* utility_weights, float* probs,
+                            float* utility, void* ws, size_t ws_bytes, void* stream) {
+    if (!m) return fail(UPR_ERR_NULL, "model is NULL");
+    if (!hd) return fail(UPR_ERR_NULL, "heads is NULL");
+    if (!same_shape(m->cfg, hd->cfg))
+        return fail(UPR_ERR_CONFIG, "heads were created for a different model shape");
+    int64_t hf, hl, cf, cl;
+    upr_status st = check_segments(hist, "hist", &hf, &hl);
+    if (st != UPR_OK) return st;
+    st = check_segments(cand, "cand", &cf, &cl);
+    if (st != UPR_OK) return st;
+    if (hist->num_users != cand->num_users)
+        return fail(UPR_ERR_OFFSETS, "hist has %d users, cand has %d", hist->num_users,
+                    cand->num_users);
+    if (!cache) return fail(UPR_ERR_NULL, "cache is NULL");
+    if (cache->capacity_rows < 0 || hl > cache->capacity_rows)
+        return fail(UPR_ERR_CAPACITY, "history rows end at %lld, cache capacity is %lld",
+                    (long long)hl, (long long)cache->capacity_rows);
+    if (!utility_weights) return fail(UPR_ERR_NULL, "utility_weights is NULL");
+    if (!probs && !utility) return fail(UPR_ERR_NULL, "probs and utility are both NULL");
+    if (cl > cf) {
+        if (!cand_emb) return fail(UPR_ERR_NULL, "cand_emb is NULL");
+        if (hl > hf && !cache->data) return fail(UPR_ERR_NULL, "cache data is NULL");
+    }
+    const upr::RankPlan p = upr::plan_rank(m->cfg, cand->num_users, cand->offsets_host, hd->C * hd->Fh);
+    st = check_workspace(ws, ws_bytes, p.bytes);
+    if (st != UPR_OK) return st;
+    if (p.rows == 0) return ok();
+    upr::RankOut out;
+    out.heads = hd;
+    for (int c = 0; c < hd->C; ++c) out.uw.u[c] = utility_weights[c];
+    out.probs = probs;
+    out.util = utility;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* w = static_cast<char*>(ws);
+    st = m->cfg.dtype == UPR_BF16
+             ? upr::run_rank<upr::Bf16Types>(m, cache, hist, static_cast<const bf16*>(cand_emb),
+                                             cand, out, p, w, s)
+             : upr::run_rank<upr::F32Types>(m, cache, hist, static_cast<const float*>(cand_emb),
+                                            cand, out, p, w, s);
+    return st == UPR_OK ? ok() : st;
+}
+
+upr_status upr_topk_by_utility(const float* utility, const upr_segments* cand, int32_t K,
+                               int32_t* topk_rows, float* topk_utility, void* stream) {
+    static_assert(upr::kTopkMaxCandidates == UPR_TOPK_MAX_CANDIDATES, "limit mismatch");
+    int64_t cf, cl;
+    upr_status st = check_segments(cand, "cand", &cf, &cl);
+    if (st != UPR_OK) return st;
+    if (K < 1) return fail(UPR_ERR_LIMIT, "K = %d < 1", K);
+    for (int u = 0; u < cand->num_users; ++u) {
+        const int32_t k = cand->offsets_host[u + 1] - cand->offsets_host[u];
+        if (k > UPR_TOPK_MAX_CANDIDATES)
+            return fail(UPR_ERR_LIMIT, "user %d has %d candidates, top-K accepts at most %d", u, k,
+                        UPR_TOPK_MAX_CANDIDATES);
+    }
+    if (cand->num_users == 0) return ok();
+    if (!topk_rows) return fail(UPR_ERR_NULL, "topk_rows is NULL");
+    if (cl > cf && !utility) return fail(UPR_ERR_NULL, "utility is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    {
+        upr::ProfScope ps("topk", s);
+        const hipError_t e = upr::launch_topk(utility, cand->offsets_dev, cand->num_users, K,
+                                              topk_rows, topk_utility, s);
+        if (e != hipSuccess) return fail(UPR_ERR_HIP, "top-K launch failed: %s", hipGetErrorString(e));
+    }
+    return ok();
 }
 
 const char* upr_status_string(int32_t s) {
@@ -582,6 +798,7 @@ const char* upr_status_string(int32_t s) {
         case UPR_ERR_DTYPE: return "unknown dtype";
         case UPR_ERR_HIP: return "HIP runtime error";
         case UPR_ERR_WEIGHTS: return "weight blob size mismatch";
+        case UPR_ERR_LIMIT: return "argument exceeds a documented limit";
         default: return "unknown status";
     }
 }

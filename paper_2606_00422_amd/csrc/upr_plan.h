@@ -1,6 +1,7 @@
 // Workspace plans of encode and rank, and the launchers they dispatch to.
 #pragma once
 
+#include <algorithm>
 #include <cstddef>
 #include <cstdint>
 
@@ -70,9 +71,10 @@ inline EncodePlan plan_encode(const upr_config& c, int U, const int32_t* hoffs) 
 }
 
 // Workspace of rank for the candidate rows of `coffs` (host offsets):
-// residual, LayerNorm output, fused q|k|v rows, attention output, FFN hidden,
-// and (bf16 models) the attention work list.
-inline RankPlan plan_rank(const upr_config& c, int U, const int32_t* coffs) {
+// residual, LayerNorm output, fused q|k|v rows, attention output, FFN hidden
+// (at least head_cols wide: the action heads' hidden layer reuses it), and
+// (bf16 models) the attention work list.
+inline RankPlan plan_rank(const upr_config& c, int U, const int32_t* coffs, int head_cols = 0) {
     RankPlan p;
     p.row0 = coffs[0];
     p.rows = (int64_t)coffs[U] - coffs[0];
@@ -85,7 +87,7 @@ inline RankPlan plan_rank(const upr_config& c, int U, const int32_t* coffs) {
     p.off_a = o; o = align256(o + R * d * es);
     p.off_qkv = o; o = align256(o + R * 3 * d * es);
     p.off_o = o; o = align256(o + R * d * es);
-    p.off_h = o; o = align256(o + R * F * es);
+    p.off_h = o; o = align256(o + R * std::max<size_t>(F, (size_t)head_cols) * es);
     p.off_work = o; o = align256(o + (size_t)p.work_items * 4 * sizeof(int32_t));
     p.bytes = o;
     return p;
@@ -121,5 +123,25 @@ hipError_t launch_attn_encode(const bf16* q, f16* o, int64_t row0, int H, int D,
                               const int32_t* hist_offsets, const int32_t* work, int64_t items,
                               int tile, const bf16* cache_k, const bf16* cache_v,
                               int64_t cache_cap, hipStream_t s);
+
+// Per-action heads: at most kMaxActions heads; utility weights by value.
+constexpr int kMaxActions = 8;
+struct HeadUtility {
+    float u[kMaxActions];
+};
+
+// logit_c = w2_c . hid[:, c*Fh .. c*Fh+Fh) + b2_c, probs[r, c] = sigmoid(logit_c)
+// (if probs), util[r] = sum_c u_c probs[r, c] (if util); hid rows of ldh
+// elements, Fh a multiple of 8.
+template <typename TA>
+hipError_t launch_heads_out(const TA* hid, int64_t ldh, int64_t rows, int C, int Fh,
+                            const float* w2, const float* b2, const HeadUtility& uw, float* probs,
+                            float* util, hipStream_t s);
+
+// Per-user top K by utility (one workgroup per user, at most
+// kTopkMaxCandidates candidates per user: the caller checks).
+constexpr int kTopkMaxCandidates = 16384;
+hipError_t launch_topk(const float* util, const int32_t* coffs_dev, int U, int K,
+                       int32_t* out_rows, float* out_util, hipStream_t s);
 
 }  // namespace upr

@@ -17,7 +17,8 @@ import numpy as np
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libupr.so")
 
 UPR_OK, UPR_ERR_NULL, UPR_ERR_CONFIG, UPR_ERR_OFFSETS, UPR_ERR_CAPACITY = 0, 1, 2, 3, 4
-UPR_ERR_WORKSPACE, UPR_ERR_DTYPE, UPR_ERR_HIP, UPR_ERR_WEIGHTS = 5, 6, 7, 8
+UPR_ERR_WORKSPACE, UPR_ERR_DTYPE, UPR_ERR_HIP, UPR_ERR_WEIGHTS, UPR_ERR_LIMIT = 5, 6, 7, 8, 9
+UPR_TOPK_MAX_CANDIDATES = 16384
 UPR_F32, UPR_BF16 = 0, 1
 
 # Every symbol include/upr.h declares.
@@ -26,6 +27,8 @@ EXPORTS = (
     "upr_kv_cache_index", "upr_encode_workspace_bytes", "upr_rank_workspace_bytes",
     "upr_encode_user", "upr_rank_candidates", "upr_status_string", "upr_last_error",
     "upr_profile_enable", "upr_profile_read",
+    "upr_heads_weights_count", "upr_heads_create", "upr_heads_destroy",
+    "upr_rank_actions_workspace_bytes", "upr_rank_actions", "upr_topk_by_utility",
 )
 
 
@@ -42,6 +45,10 @@ class upr_segments(ctypes.Structure):
 
 class upr_kv_cache(ctypes.Structure):
     _fields_ = [("data", ctypes.c_void_p), ("capacity_rows", ctypes.c_int64)]
+
+
+class upr_heads_config(ctypes.Structure):
+    _fields_ = [("n_actions", ctypes.c_int32), ("hidden", ctypes.c_int32)]
 
 
 class upr_kernel_stat(ctypes.Structure):
@@ -83,6 +90,12 @@ def load(path: str = LIB_PATH):
         "upr_last_error": (ctypes.c_char_p, []),
         "upr_profile_enable": (I32, [I32]),
         "upr_profile_read": (I32, [P(upr_kernel_stat), I32]),
+        "upr_heads_weights_count": (I64, [cfgp, P(upr_heads_config)]),
+        "upr_heads_create": (I32, [VP, P(upr_heads_config), VP, I64, P(VP)]),
+        "upr_heads_destroy": (None, [VP]),
+        "upr_rank_actions_workspace_bytes": (SZ, [VP, VP, segp, segp]),
+        "upr_rank_actions": (I32, [VP, VP, cachep, segp, VP, segp, VP, VP, VP, VP, SZ, VP]),
+        "upr_topk_by_utility": (I32, [VP, segp, I32, VP, VP, VP]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -151,6 +164,42 @@ def upr_rank_candidates(model, cache: upr_kv_cache, hist: upr_segments, cand_emb
                         cand: upr_segments, scores_ptr, ws_ptr, ws_bytes, stream) -> None:
     _check(load().upr_rank_candidates(model, ctypes.byref(cache), ctypes.byref(hist), cand_emb_ptr,
                                       ctypes.byref(cand), scores_ptr, ws_ptr, ws_bytes, stream))
+
+
+def upr_heads_weights_count(cfg: upr_config, hc: upr_heads_config) -> int:
+    return int(load().upr_heads_weights_count(ctypes.byref(cfg), ctypes.byref(hc)))
+
+
+def upr_heads_create(model: int, hc: upr_heads_config, weights: np.ndarray) -> int:
+    w = np.ascontiguousarray(weights, dtype=np.float32)
+    out = ctypes.c_void_p()
+    _check(load().upr_heads_create(model, ctypes.byref(hc), w.ctypes.data, w.size, ctypes.byref(out)))
+    return int(out.value)
+
+
+def upr_heads_destroy(heads: int) -> None:
+    load().upr_heads_destroy(heads)
+
+
+def upr_rank_actions_workspace_bytes(model: int, heads: int, hist: upr_segments,
+                                     cand: upr_segments) -> int:
+    return int(load().upr_rank_actions_workspace_bytes(model, heads, ctypes.byref(hist),
+                                                       ctypes.byref(cand)))
+
+
+def upr_rank_actions(model, heads, cache: upr_kv_cache, hist: upr_segments, cand_emb_ptr,
+                     cand: upr_segments, utility_weights: np.ndarray, probs_ptr, utility_ptr,
+                     ws_ptr, ws_bytes, stream) -> None:
+    uw = np.ascontiguousarray(utility_weights, dtype=np.float32)
+    _check(load().upr_rank_actions(model, heads, ctypes.byref(cache), ctypes.byref(hist),
+                                   cand_emb_ptr, ctypes.byref(cand), uw.ctypes.data, probs_ptr,
+                                   utility_ptr, ws_ptr, ws_bytes, stream))
+
+
+def upr_topk_by_utility(utility_ptr, cand: upr_segments, K: int, rows_ptr, values_ptr,
+                        stream) -> None:
+    _check(load().upr_topk_by_utility(utility_ptr, ctypes.byref(cand), K, rows_ptr, values_ptr,
+                                      stream))
 
 
 def upr_status_string(status: int) -> str:
@@ -263,3 +312,58 @@ class Model:
         upr_rank_candidates(self.handle, kv, hs, cand_emb.data_ptr(), cs, scores.data_ptr(),
                             ws.data_ptr(), ws.numel(), current_stream() if stream is None else stream)
         return ws
+
+    def rank_actions(self, heads: "Heads", cache, hist_off_host, hist_off_dev, cand_emb,
+                     cand_off_host, cand_off_dev, utility_weights, probs=None, utility=None,
+                     ws=None, stream=None):
+        """upr_rank_actions on tensors: probs [rows, C] and/or utility [rows]
+        (float32 GPU tensors indexed like cand_emb rows)."""
+        _check_tensor(cand_emb, "cand_emb", self.torch_dtype)
+        _check_tensor(cache, "cache", self.torch_dtype)
+        if probs is not None:
+            _check_tensor(probs, "probs", "float32")
+        if utility is not None:
+            _check_tensor(utility, "utility", "float32")
+        hs = segments(hist_off_host, hist_off_dev)
+        cs = segments(cand_off_host, cand_off_dev)
+        need = upr_rank_actions_workspace_bytes(self.handle, heads.handle, hs, cs)
+        if ws is None:
+            ws = self.workspace(need)
+        kv = upr_kv_cache(cache.data_ptr(), cache.shape[3])
+        upr_rank_actions(self.handle, heads.handle, kv, hs, cand_emb.data_ptr(), cs,
+                         np.asarray(utility_weights, dtype=np.float32),
+                         0 if probs is None else probs.data_ptr(),
+                         0 if utility is None else utility.data_ptr(),
+                         ws.data_ptr(), ws.numel(), current_stream() if stream is None else stream)
+        return ws
+
+
+class Heads:
+    """Per-action heads created for a model (upr_heads_create)."""
+
+    def __init__(self, model: Model, n_actions: int, hidden: int, weights: np.ndarray):
+        self.cfg = upr_heads_config(n_actions, hidden)
+        self.handle = upr_heads_create(model.handle, self.cfg, weights)
+
+    def close(self):
+        if self.handle:
+            upr_heads_destroy(self.handle)
+            self.handle = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def topk(utility, cand_off_host, cand_off_dev, K, rows, values=None, stream=None):
+    """upr_topk_by_utility on tensors: rows int32 [U, K], values float32 [U, K]."""
+    _check_tensor(utility, "utility", "float32")
+    _check_tensor(rows, "rows", "int32")
+    if values is not None:
+        _check_tensor(values, "values", "float32")
+    cs = segments(cand_off_host, cand_off_dev)
+    upr_topk_by_utility(utility.data_ptr(), cs, int(K), rows.data_ptr(),
+                        0 if values is None else values.data_ptr(),
+                        current_stream() if stream is None else stream)

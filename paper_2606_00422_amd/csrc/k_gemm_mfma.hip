@@ -19,11 +19,12 @@
 //
 // Epilogue.  Stores straight from the MFMA layout touch 32 rows per
 // instruction with 8-16 bytes each and reach about 60% of the bandwidth of
-// row-contiguous stores.  Each wave therefore stages its results through its
-// own LDS region, 32 rows at a time, and writes full 128-byte (16-bit output)
-// or 256-byte (fp32 residual) row segments, 16 bytes per lane.  The stores
-// are non-temporal, so the output stream does not evict the operand panels
-// that later tiles re-read from L2.
+// row-contiguous stores.  Each wave therefore stages its raw accumulators
+// through its own LDS region, 32 rows at a time, and applies scale, bias and
+// the epilogue operation on the row-contiguous read-back, writing full
+// 256-byte (fp32 residual) or 128-byte (16-bit output) row segments.  The
+// stores are non-temporal, so the output stream does not evict the operand
+// panels that later tiles re-read from L2.
 //
 // Tile order is XCD-aware: workgroup b runs on XCD b % 8 and the tiles are
 // renumbered so each XCD sweeps a contiguous range of (M-panel, N-tile)
@@ -48,11 +49,11 @@ constexpr int kTM = kWM / 32, kTN = kWN / 32;      // 32x32 MFMA tiles per wave
 constexpr int kCPR = kBK / 8;                      // 16-byte chunks per LDS row (8)
 constexpr int kLoadsA = 2 * kBM * kCPR / kThreads; // per leading wave per K-step (8)
 constexpr int kLoadsB = 2 * kBN * kCPR / kThreads;
-// Epilogue staging row strides (elements).  16-bit: 144 bytes, so the 16
-// rows written by one 16-lane group of 16-byte stores fall on distinct bank
-// groups and rows 8 apart on disjoint halves; fp32: 272 bytes, likewise for
-// the 16-byte fp32 writes.
-constexpr int kStage16 = 72, kStage32 = 68;
+// Epilogue staging row strides (elements).  fp32: 272 bytes, so the 16 rows
+// written by one 16-lane group of 16-byte stores fall on distinct bank
+// groups; 16-bit: 144 bytes, likewise, and rows 8 apart land on disjoint
+// halves.
+constexpr int kStage32 = 68, kStage16 = 72;
 constexpr int kRegionBytes = 16384;                // LDS staging region per wave
 
 __device__ __forceinline__ int xcd_tile(int b, int nb) {
@@ -97,78 +98,82 @@ __device__ __forceinline__ unsigned pack2(float a, float b) {
 // Epilogue of one wave's 128 x 64 tile (acc in the transposed MFMA layout:
 // register r of tile (j, i) holds row 32i + lane%32 and column
 // 32j + 8(r/4) + 4(lane/32) + r%4 of the wave tile at (wrow0, wcol0)),
-// staged through the wave's own LDS region (fp32 residual passes of RROWS
-// rows: RROWS x 272 bytes; 16-bit passes of 32 rows: 32 x 144 bytes; the
-// region must hold the larger).
-template <int MODE, int RROWS>
+// 32 rows at a time through the wave's own LDS region.
+//
+// fp32 residual update: the raw accumulators are staged (32 x 272 bytes)
+// and come back row-contiguous, lane l holding columns 4(l%16) .. +3 of rows
+// 4p + l/16, p = 0..7: the bias is one float4 per lane loaded before the
+// first pass, each store covers 256-byte row segments, and the residual
+// rows of the next pass are loaded while this one is processed.
+//
+// 16-bit outputs: scale, bias and the operation are applied in the MFMA
+// layout; after conversion lane pairs (l, l+32) exchange halves with
+// v_permlane32_swap so each lane holds eight consecutive columns (16 bytes)
+// and the staged rows (32 x 144 bytes) are written back as 128-byte
+// segments, 16 bytes per lane (narrower stores measured slower).
+template <int MODE>
 __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* const region,
                                            int64_t wrow0, int wcol0, int64_t M, int N,
                                            const Epilogue& epi, int lane) {
     const int lrow = lane & 31, lhalf = lane >> 5;
-    float4 bq[kTN][4];
-#pragma unroll
-    for (int j = 0; j < kTN; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int col = wcol0 + j * 32 + 8 * q + 4 * lhalf;
-            bq[j][q] = col < N ? *reinterpret_cast<const float4*>(epi.bias + col)
-                               : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
     const float sc = epi.acc_scale;
-
     if constexpr (MODE == EPI_RESID) {
-        // fp32 staging: a lane writes its four-column runs (16 bytes); reads
-        // give 16 lanes per 256-byte row segment, 4 rows per instruction.
-        float* const st = reinterpret_cast<float*>(region);
-        const int ch = lane & 15;
+        const int ch = lane & 15, rsub = lane >> 4;
         const int col = wcol0 + ch * 4;
-        constexpr int kPasses = 32 / RROWS;
+        const bool col_ok = col < N;                  // N is a multiple of 8
+        const float4 bias4 = col_ok ? *reinterpret_cast<const float4*>(epi.bias + col)
+                                    : make_float4(0.f, 0.f, 0.f, 0.f);
+        float* const st = reinterpret_cast<float*>(region);
+        float4 g[8], gn[8];
+        auto load_resid = [&](int i, float4 (&dst)[8]) {
+#pragma unroll
+            for (int p = 0; p < 8; ++p) {
+                const int64_t row = wrow0 + i * 32 + p * 4 + rsub;
+                if (row < M && col_ok)
+                    dst[p] = *reinterpret_cast<const float4*>(epi.resid + row * epi.ldr + col);
+            }
+        };
+        load_resid(0, g);
 #pragma unroll
         for (int i = 0; i < kTM; ++i) {
 #pragma unroll
-            for (int hp = 0; hp < kPasses; ++hp) {
-                if (lrow / RROWS == hp) {
+            for (int j = 0; j < kTN; ++j)
 #pragma unroll
-                    for (int j = 0; j < kTN; ++j)
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            float4 v;
-                            v.x = fmaf(acc[j][i][4 * q + 0], sc, bq[j][q].x);
-                            v.y = fmaf(acc[j][i][4 * q + 1], sc, bq[j][q].y);
-                            v.z = fmaf(acc[j][i][4 * q + 2], sc, bq[j][q].z);
-                            v.w = fmaf(acc[j][i][4 * q + 3], sc, bq[j][q].w);
-                            *reinterpret_cast<float4*>(st + (lrow % RROWS) * kStage32 + j * 32 + 8 * q + 4 * lhalf) = v;
-                        }
+                for (int q = 0; q < 4; ++q) {
+                    const float4 v = make_float4(acc[j][i][4 * q + 0], acc[j][i][4 * q + 1],
+                                                 acc[j][i][4 * q + 2], acc[j][i][4 * q + 3]);
+                    *reinterpret_cast<float4*>(st + lrow * kStage32 + j * 32 + 8 * q + 4 * lhalf) = v;
                 }
-                __builtin_amdgcn_s_waitcnt(0xC07F);
-                __builtin_amdgcn_wave_barrier();
-                float4 x[RROWS / 4], g[RROWS / 4];
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            __builtin_amdgcn_wave_barrier();
+            if (i + 1 < kTM) load_resid(i + 1, gn);
+            float4 x[8];
 #pragma unroll
-                for (int p = 0; p < RROWS / 4; ++p) {
-                    const int rl = p * 4 + (lane >> 4);
-                    const int64_t row = wrow0 + i * 32 + hp * RROWS + rl;
-                    x[p] = *reinterpret_cast<const float4*>(st + rl * kStage32 + ch * 4);
-                    if (row < M && col < N)
-                        g[p] = *reinterpret_cast<const float4*>(epi.resid + row * epi.ldr + col);
-                }
+            for (int p = 0; p < 8; ++p)
+                x[p] = *reinterpret_cast<const float4*>(st + (p * 4 + rsub) * kStage32 + ch * 4);
 #pragma unroll
-                for (int p = 0; p < RROWS / 4; ++p) {
-                    const int64_t row = wrow0 + i * 32 + hp * RROWS + p * 4 + (lane >> 4);
-                    if (row >= M || col >= N) continue;
-                    float4 o = g[p];
-                    o.x += x[p].x; o.y += x[p].y; o.z += x[p].z; o.w += x[p].w;
-                    __builtin_nontemporal_store(f32x4{o.x, o.y, o.z, o.w}, reinterpret_cast<f32x4*>(epi.resid + row * epi.ldr + col));
-                }
-                __builtin_amdgcn_s_waitcnt(0xC07F);
-                __builtin_amdgcn_wave_barrier();
+            for (int p = 0; p < 8; ++p) {
+                const int64_t row = wrow0 + i * 32 + p * 4 + rsub;
+                if (row >= M || !col_ok) continue;
+                const f32x4 o = {g[p].x + fmaf(x[p].x, sc, bias4.x), g[p].y + fmaf(x[p].y, sc, bias4.y),
+                                 g[p].z + fmaf(x[p].z, sc, bias4.z), g[p].w + fmaf(x[p].w, sc, bias4.w)};
+                __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(epi.resid + row * epi.ldr + col));
             }
+#pragma unroll
+            for (int p = 0; p < 8; ++p) g[p] = gn[p];
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            __builtin_amdgcn_wave_barrier();
         }
     } else {
-        // 16-bit staging.  After conversion, lane pairs (l, l+32) exchange
-        // halves with v_permlane32_swap so each lane holds eight consecutive
-        // columns (16 bytes): lane l gets columns 16c + 8(l/32) + 0..7, c = 0, 1,
-        // of each 32-column tile.  Reads give 8 lanes per 128-byte row
-        // segment; the two rows of a 16-lane group are 8 apart (bank-disjoint).
+        float4 bq[kTN][4];
+#pragma unroll
+        for (int j = 0; j < kTN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int col = wcol0 + j * 32 + 8 * q + 4 * lhalf;
+                bq[j][q] = col < N ? *reinterpret_cast<const float4*>(epi.bias + col)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
         constexpr bool kBf = MODE != EPI_GELU;
         unsigned short* const st = reinterpret_cast<unsigned short*>(region);
         const int ch = lane & 7, rs = lane >> 3;
@@ -381,7 +386,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict
     const int wsel = __builtin_amdgcn_readfirstlane(wave) >> 1;
     f16* const sbase = wsel == 0 ? sA0 : wsel == 1 ? sA1 : wsel == 2 ? sB0 : sB1;
     char* const region = reinterpret_cast<char*>(sbase) + (wave & 1) * kRegionBytes;
-    store_tile<MODE, 32>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane);
+    store_tile<MODE>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane);
     if (lead) __builtin_amdgcn_s_barrier();
 }
 

@@ -12,7 +12,9 @@ Prints one JSON line.  Besides the contract fields it carries:
                   profiled pass over the same steps), against MI355X's peak;
   cpu_baseline  - the CPU oracle ranking a bounded sample of the same
                   workload on this host's cores;
-  path_mfma_frac, p50/p90 single-user latency, encode time, per-kernel times.
+  path_mfma_frac, p10/p50/p90 of the timed steps, p50/p90 single-user latency
+  (eager calls, and the same calls replayed from HIP graphs), encode time,
+  per-kernel times.
 """
 from __future__ import annotations
 
@@ -84,22 +86,37 @@ def path_flops(inp):
     return L * (R * (8 * d * d + 4 * d * F) + 4 * d * pairs) + 2 * d * R
 
 
-def cpu_baseline(inp, budget_s=12.0):
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(inp, budget_s=12.0, single_users=2):
     """Oracle rank on a bounded sample of users (its cache from oracle.encode,
-    untimed: encoding is the step before ranking)."""
+    untimed: encoding is the step before ranking), with the BLAS pool as it
+    comes; then single-threaded on `single_users` of those users,
+    extrapolated to the whole workload."""
     import oracle
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
         blas = ",".join(sorted({i.get("internal_api", "?") for i in threadpool_info()}))
     except Exception:
+        threadpool_limits = None
         threads, blas = os.cpu_count() or 1, "unknown"
-    done_users, cands, t_rank = [], 0, 0.0
+    done_users, cands, t_rank, caches = [], 0, 0.0, {}
     order = np.argsort(-inp.cand_lens, kind="stable")        # typical users first
     order = order[len(order) // 2:].tolist() + order[: len(order) // 2].tolist()
     for u in order:
         cache = oracle.encode(inp.weights, inp.d, inp.H, inp.L, inp.F, inp.hist_emb,
                               inp.hist_offsets, users=[u])
+        if len(caches) < single_users:
+            caches[int(u)] = cache
         t0 = time.perf_counter()
         oracle.rank(inp.weights, inp.d, inp.H, inp.L, inp.F, cache, inp.hist_offsets,
                     inp.cand_emb, inp.cand_offsets, users=[u])
@@ -108,10 +125,25 @@ def cpu_baseline(inp, budget_s=12.0):
         cands += int(inp.cand_lens[u])
         if t_rank >= budget_s:
             break
-    return {"value": cands / t_rank, "unit": "candidate scores/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"oracle.rank (numpy float64, BLAS {blas}) over {len(done_users)} of "
-                      f"{inp.U} users ({cands} candidates), {t_rank:.1f} s"}
+    out = {"value": cands / t_rank, "unit": "candidate scores/s", "cores": int(threads),
+           "kind": "oracle", "cpu": cpu_model(), "blas": blas,
+           "sample": f"oracle.rank (numpy float64, BLAS {blas}) over {len(done_users)} of "
+                     f"{inp.U} users ({cands} candidates), {t_rank:.1f} s"}
+    if threadpool_limits is not None and caches:
+        c1, t1 = 0, 0.0
+        with threadpool_limits(limits=1):
+            for u, cache in caches.items():
+                t0 = time.perf_counter()
+                oracle.rank(inp.weights, inp.d, inp.H, inp.L, inp.F, cache, inp.hist_offsets,
+                            inp.cand_emb, inp.cand_offsets, users=[u])
+                t1 += time.perf_counter() - t0
+                c1 += int(inp.cand_lens[u])
+        total = float(inp.cand_offsets[-1] - inp.cand_offsets[0])
+        out["single_thread"] = {
+            "value": c1 / t1, "unit": "candidate scores/s", "cores": 1,
+            "sample": f"{len(caches)} users ({c1} candidates), {t1:.1f} s",
+            "extrapolated_workload_s": round(t1 * total / c1, 1)}
+    return out
 
 
 def actions_topk(args, inp, model, kv, hs, cs, C, Kc, ev, stream):
@@ -174,6 +206,9 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-actions", action="store_true",
                     help="skip the per-action heads + utility top-K measurement")
+    ap.add_argument("--flush-mall", action="store_true",
+                    help="write a 512 MiB scratch buffer before every rank step (evicts the "
+                         "256 MB MALL; for counter runs, not for the headline number)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this path has no "
@@ -207,9 +242,13 @@ def main():
     def encode():
         upr.upr_encode_user(model.handle, X.data_ptr(), hs, kv, ws.data_ptr(), ws.numel(), stream)
 
-    def rank(h=hs, c=cs):
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda") if args.flush_mall else None
+
+    def rank(h=hs, c=cs, st=None):
+        if flush is not None and st is None:
+            flush.fill_(1)
         upr.upr_rank_candidates(model.handle, kv, h, C.data_ptr(), c, scores.data_ptr(),
-                                ws.data_ptr(), ws.numel(), stream)
+                                ws.data_ptr(), ws.numel(), stream if st is None else st)
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
     encode()
@@ -224,15 +263,16 @@ def main():
     for _ in range(args.warmup):
         rank()
     torch.cuda.synchronize()
-    # timed region (no per-kernel events inside)
-    e0, e1 = ev(), ev()
+    # timed region: one event between consecutive steps (no per-kernel events)
+    evs = [ev() for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    e0.record()
-    for _ in range(args.steps):
+    evs[0].record()
+    for i in range(args.steps):
         rank()
-    e1.record()
+        evs[i + 1].record()
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
     assert bool(torch.isfinite(scores[:Kc]).all()), "non-finite scores"
 
     # profiled pass over the same steps: per-kernel HIP events on the stream
@@ -285,6 +325,32 @@ def main():
             lat.append(a.elapsed_time(b))
     lat = np.array(lat) if lat else np.array([np.nan])
 
+    # the same single-user calls captured once each into a HIP graph and
+    # replayed; every replay is checked bit for bit against the eager result
+    # (the user's scores are overwritten with NaN between replays)
+    glat = []
+    for u in range(inp.U if args.user_reps > 0 else 0):
+        h1 = upr.segments(np.ascontiguousarray(hoff[u:u + 2]), hoff_d[u:u + 2])
+        c1 = upr.segments(np.ascontiguousarray(coff[u:u + 2]), coff_d[u:u + 2])
+        sl = slice(int(coff[u]), int(coff[u + 1]))
+        rank(h1, c1)
+        torch.cuda.synchronize()
+        ref = scores[sl].clone()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            rank(h1, c1, upr.current_stream())
+        for _ in range(args.user_reps):
+            scores[sl].fill_(float("nan"))
+            a, b = ev(), ev()
+            a.record()
+            g.replay()
+            b.record()
+            torch.cuda.synchronize()
+            glat.append(a.elapsed_time(b))
+            assert torch.equal(scores[sl], ref), f"graph replay of user {u} differs from eager"
+        del g
+    glat = np.array(glat) if glat else np.array([np.nan])
+
     flops = path_flops(inp)
     out = {
         "metric": "candidate scores/sec (1 GPU)",
@@ -295,14 +361,20 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16+fp16" if inp.dtype == "bf16" else "f32",
         "data": "synthetic",
-        "config": {"workload": args.workload, "users": inp.U,
+        "config": {"workload": args.workload, "users": inp.U, "flush_mall": bool(args.flush_mall),
                    "history_rows": T, "candidate_rows": Kc, "d_model": inp.d,
                    "heads": inp.H, "layers": inp.L, "d_ff": inp.F},
         "path_tflops": round(flops / (ms * 1e-3) / 1e12, 2),
         "path_mfma_frac": round(flops / (ms * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
+        "step_ms": {"p10": round(float(np.percentile(per_step, 10)), 4),
+                    "p50": round(float(np.percentile(per_step, 50)), 4),
+                    "p90": round(float(np.percentile(per_step, 90)), 4)},
         "user_latency_ms": {"p50": round(float(np.percentile(lat, 50)), 4),
                             "p90": round(float(np.percentile(lat, 90)), 4),
                             "calls": int(lat.size)},
+        "user_latency_graph_ms": {"p50": round(float(np.percentile(glat, 50)), 4),
+                                  "p90": round(float(np.percentile(glat, 90)), 4),
+                                  "replays": int(glat.size)},
         "encode_ms": round(encode_ms, 3),
         "roofline": roof,
         "kernels": kernels,

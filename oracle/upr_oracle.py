@@ -125,10 +125,11 @@ def masked_softmax_attention(q, k, v, allowed):
     return p @ v
 
 
-def ffn(x, lw):
+def ffn(x, lw, lin=None):
     """Feed-forward sub-block input -> LN2 -> W1 -> GELU -> W2 (no residual)."""
     a = layer_norm(x, lw["ln2_g"], lw["ln2_b"])
-    return linear(gelu_tanh(linear(a, lw["W1"], lw["b1"])), lw["W2"], lw["b2"])
+    lin = linear if lin is None else lin
+    return lin(gelu_tanh(lin(a, lw["W1"], lw["b1"])), lw["W2"], lw["b2"])
 
 
 def score_head(h, final):
@@ -218,8 +219,22 @@ def encode(blob, d, H, L, F, hist_emb, hist_offsets, capacity_rows=None, users=N
     return cache
 
 
+def _projection_rule(proj):
+    """(linear map, what the O projection's input goes through first) for the
+    exact model or the MXFP8 projection variant (oracle/upr_mx.py): every
+    projection input and weight MXFP8-encoded along the contraction axis, the
+    attention output first held in bf16 (the precision it is materialised
+    in before it is encoded)."""
+    if proj == "exact":
+        return linear, (lambda o: o)
+    if proj == "mxfp8":
+        from .upr_mx import bf16_round, linear_mx
+        return linear_mx, bf16_round
+    raise ValueError(f"unknown projection rule {proj!r}")
+
+
 def rank_hidden(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
-                users=None, cand_rows=None):
+                users=None, cand_rows=None, proj="exact"):
     """Candidate forward pass against the cached history (Sec. 3, serving
     design and KV-cache sharing): only candidate tokens are processed.
 
@@ -232,8 +247,10 @@ def rank_hidden(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
     Returns the float64 final hidden states g [rows, d] of every packed
     candidate row (NaN for rows not requested).  ``users`` and ``cand_rows``
     (absolute packed row indices) restrict the work; candidates are
-    independent, so a subset is exact.
+    independent, so a subset is exact.  ``proj="mxfp8"`` runs the four
+    projections of every layer in MXFP8 (see ``_projection_rule``).
     """
+    lin, o_in = _projection_rule(proj)
     layers, final = unpack_weights(blob, d, L, F)
     D = d // H
     hoffs = np.asarray(hist_offsets, dtype=np.int64)
@@ -254,9 +271,9 @@ def rank_hidden(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
         kc_rows = rows.size
         for l, lw in enumerate(layers):
             a = layer_norm(g, lw["ln1_g"], lw["ln1_b"])
-            q = _split_heads(linear(a, lw["Wq"], lw["bq"]), H)
-            ks = _split_heads(linear(a, lw["Wk"], lw["bk"]), H)
-            vs = _split_heads(linear(a, lw["Wv"], lw["bv"]), H)
+            q = _split_heads(lin(a, lw["Wq"], lw["bq"]), H)
+            ks = _split_heads(lin(a, lw["Wk"], lw["bk"]), H)
+            vs = _split_heads(lin(a, lw["Wv"], lw["bv"]), H)
             o = np.empty((H, kc_rows, D))
             for j in range(H):
                 Kh = cache[l, 0, j, lo:hi, :]          # [n_u, D]
@@ -268,19 +285,19 @@ def rank_hidden(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
                 p = np.exp(s - m)
                 p = p / p.sum(axis=1, keepdims=True)
                 o[j] = p[:, :-1] @ Vh + p[:, -1:] * vs[j]
-            g = g + linear(o.transpose(1, 0, 2).reshape(kc_rows, d), lw["Wo"], lw["bo"])
-            g = g + ffn(g, lw)
+            g = g + lin(o_in(o.transpose(1, 0, 2).reshape(kc_rows, d)), lw["Wo"], lw["bo"])
+            g = g + ffn(g, lw, lin)
         hidden[rows] = g
     return hidden
 
 
 def rank(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
-         users=None, cand_rows=None):
+         users=None, cand_rows=None, proj="exact"):
     """Candidate scores w . LN_f(g) + b of the final hidden states
     (``rank_hidden``); float64, NaN for rows not requested."""
     _, final = unpack_weights(blob, d, L, F)
     g = rank_hidden(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
-                    users=users, cand_rows=cand_rows)
+                    users=users, cand_rows=cand_rows, proj=proj)
     scores = np.full(g.shape[0], np.nan)
     ok = ~np.isnan(g[:, 0]) if g.shape[0] else np.zeros(0, dtype=bool)
     scores[ok] = score_head(g[ok], final)

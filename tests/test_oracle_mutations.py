@@ -24,10 +24,10 @@ MUTATIONS = {
                                      "causal = np.tril(np.ones((n, n), dtype=bool), -1) | (np.arange(n)[:, None] == 0)"),
     "mask lets candidates see each other": ("cand_row = (i >= n) & ((j < n) | (j == i))",
                                             "cand_row = (i >= n) & (j <= i)"),
-    "Wo transposed in rank": ("g = g + linear(o.transpose(1, 0, 2).reshape(kc_rows, d), lw[\"Wo\"], lw[\"bo\"])",
-                              "g = g + linear(o.transpose(1, 0, 2).reshape(kc_rows, d), lw[\"Wo\"].T, lw[\"bo\"])"),
-    "value bias dropped in rank": ("vs = _split_heads(linear(a, lw[\"Wv\"], lw[\"bv\"]), H)",
-                                   "vs = _split_heads(linear(a, lw[\"Wv\"], 0.0), H)"),
+    "Wo transposed in rank": ("g = g + lin(o_in(o.transpose(1, 0, 2).reshape(kc_rows, d)), lw[\"Wo\"], lw[\"bo\"])",
+                              "g = g + lin(o_in(o.transpose(1, 0, 2).reshape(kc_rows, d)), lw[\"Wo\"].T, lw[\"bo\"])"),
+    "value bias dropped in rank": ("vs = _split_heads(lin(a, lw[\"Wv\"], lw[\"bv\"]), H)",
+                                   "vs = _split_heads(lin(a, lw[\"Wv\"], 0.0), H)"),
     "gelu constant": ("0.044715", "0.04715"),
     "unbiased variance": ("var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)",
                           "var = ((x - mu) ** 2).sum(axis=-1, keepdims=True) / (x.shape[-1] - 1)"),
@@ -35,7 +35,7 @@ MUTATIONS = {
     "head split transposed": ("return x.reshape(rows, H, d // H).transpose(1, 0, 2)",
                               "return x.reshape(rows, d // H, H).transpose(2, 0, 1)"),
     "score bias dropped": ("@ final[\"w_score\"] + final[\"b_score\"]", "@ final[\"w_score\"]"),
-    "ffn residual sign": ("g = g + ffn(g, lw)", "g = g - ffn(g, lw)"),
+    "ffn residual sign": ("g = g + ffn(g, lw, lin)", "g = g - ffn(g, lw, lin)"),
     "cache index kv/head swapped": ("return (((layer * 2 + kv) * H + head) * capacity_rows + row) * D + e",
                                     "return (((layer * H + head) * 2 + kv) * capacity_rows + row) * D + e"),
     "encode stores pre-projection keys": ("cache[l, 0, :, lo:hi, :] = k", "cache[l, 0, :, lo:hi, :] = q"),

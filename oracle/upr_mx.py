@@ -104,13 +104,10 @@ def mx_round(x):
     return mx_dequantize(*mx_quantize(x))
 
 
-def bf16_round(x):
-    """x rounded to bfloat16 as a GPU rounds an fp32 value: to fp32 first,
-    then to the nearest bf16, ties to even."""
-    f = np.asarray(x, dtype=np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
-    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+def f16_round(x):
+    """x rounded to IEEE half precision as a GPU rounds an fp32 value: to
+    fp32 first, then to the nearest fp16, ties to even (numpy's casts)."""
+    return np.asarray(x, dtype=np.float32).astype(np.float16).astype(np.float64)
 
 
 def linear_mx(x, W, b):

@@ -223,13 +223,13 @@ def _projection_rule(proj):
     """(linear map, what the O projection's input goes through first) for the
     exact model or the MXFP8 projection variant (oracle/upr_mx.py): every
     projection input and weight MXFP8-encoded along the contraction axis, the
-    attention output first held in bf16 (the precision it is materialised
+    attention output first held in fp16 (the precision it is materialised
     in before it is encoded)."""
     if proj == "exact":
         return linear, (lambda o: o)
     if proj == "mxfp8":
-        from .upr_mx import bf16_round, linear_mx
-        return linear_mx, bf16_round
+        from .upr_mx import f16_round, linear_mx
+        return linear_mx, f16_round
     raise ValueError(f"unknown projection rule {proj!r}")
 
 

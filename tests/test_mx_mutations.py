@@ -29,7 +29,8 @@ MUTATIONS = {
     "no saturation (NaN code)": ("    return (code | sign).astype(np.uint8)",
                                  "    code = np.where(np.abs(x) > 464.0, 0x7F, code)\n    return (code | sign).astype(np.uint8)"),
     "zero block exponent 0": ("e = np.where(amax > 0, e, -127.0)", "e = np.where(amax > 0, e, 0.0)"),
-    "bf16 truncation": ("u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000", "u = u & 0xFFFF0000"),
+    "fp16 step skipped": ("return np.asarray(x, dtype=np.float32).astype(np.float16).astype(np.float64)",
+                          "return np.asarray(x, dtype=np.float64)"),
     "activation blocks across rows": ("return mx_round(x) @ mx_round(W).T", "return mx_round(x.T).T @ mx_round(W).T"),
     "weights not encoded": ("return mx_round(x) @ mx_round(W).T", "return mx_round(x) @ W.T"),
 }
@@ -45,7 +46,7 @@ PINS = [
     pins.test_representable_blocks_round_trip_exactly,
     pins.test_error_within_half_an_element_ulp,
     pins.test_all_zero_and_mixed_sign_blocks,
-    pins.test_bf16_round_matches_torch,
+    pins.test_f16_round_matches_torch,
     pins.test_linear_mx_matches_torch_fp8_when_every_scale_is_one,
     pins.test_linear_mx_on_representable_operands_is_exact,
     pins.test_mxfp8_rank_is_per_candidate,
@@ -68,7 +69,7 @@ def _failures(mod, monkeypatch):
     monkeypatch.setattr(pins, "mx_oracle", mod)
     real_rule = uo._projection_rule
     monkeypatch.setattr(uo, "_projection_rule",
-                        lambda proj: (mod.linear_mx, mod.bf16_round) if proj == "mxfp8" else real_rule(proj))
+                        lambda proj: (mod.linear_mx, mod.f16_round) if proj == "mxfp8" else real_rule(proj))
     failed = 0
     for pin in PINS:
         try:

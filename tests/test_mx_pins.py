@@ -108,11 +108,11 @@ def test_all_zero_and_mixed_sign_blocks():
     assert s[0] == 127 and c[0] == m.e4m3_round_codes(300.0) and c[1] == 0x80
 
 
-def test_bf16_round_matches_torch():
-    x = np.concatenate([RNG.standard_normal(20000) * np.exp2(RNG.integers(-30, 30, 20000)),
-                        [0.0, -0.0, 1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8]])
-    ref = torch.tensor(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
-    np.testing.assert_array_equal(mx_oracle.bf16_round(x), ref)
+def test_f16_round_matches_torch():
+    x = np.concatenate([RNG.standard_normal(20000) * np.exp2(RNG.integers(-20, 15, 20000)),
+                        [0.0, -0.0, 1.0 + 2.0 ** -11, 1.0 + 3 * 2.0 ** -11, 65504.0]])
+    ref = torch.tensor(x.astype(np.float32)).to(torch.float16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(mx_oracle.f16_round(x), ref)
 
 
 def test_linear_mx_matches_torch_fp8_when_every_scale_is_one():

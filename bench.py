@@ -195,6 +195,52 @@ def actions_topk(args, inp, model, kv, hs, cs, C, Kc, ev, stream):
             "utility_weights": list(DEFAULT_UTILITY), "extra_kernels_avg_ms": extra}
 
 
+def mxfp8_rank(args, inp, kv, hs, cs, C, Kc, ev, stream, work):
+    """The fp8 projection variant (paper Sec. 3, FP8 quantization; NEXT-3):
+    the same rank call on a UPR_BF16_MXFP8 model of the same weights, reusing
+    the cache (encode is unchanged).  Reported beside the headline, never as
+    it: the headline workload is bf16."""
+    import torch
+    from paper_2606_00422_amd import upr
+    cfg = upr.make_config(inp.d, inp.H, inp.L, inp.F, "bf16_mxfp8")
+    model = upr.Model(cfg, inp.weights)
+    scores = torch.empty(max(Kc, 1), dtype=torch.float32, device="cuda")
+    ws = model.workspace(upr.upr_rank_workspace_bytes(model.handle, hs, cs))
+
+    def step():
+        upr.upr_rank_candidates(model.handle, kv, hs, C.data_ptr(), cs, scores.data_ptr(),
+                                ws.data_ptr(), ws.numel(), stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = ev(), ev()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    assert bool(torch.isfinite(scores[:Kc]).all()), "non-finite fp8 scores"
+    upr.upr_profile_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    prof = upr.upr_profile_read()
+    upr.upr_profile_enable(False)
+    model.close()
+    kernels = {}
+    for name, (launches, total) in sorted(prof.items()):
+        avg = total / launches
+        entry = {"launches_per_step": launches / args.steps, "avg_ms": round(avg, 5)}
+        if name in work and work[name][0] == "mfma":
+            entry["tflops"] = round(work[name][1] / (avg * 1e-3) / 1e12, 2)
+        kernels[name] = entry
+    return {"ms_per_step": round(ms, 4), "candidates_per_s": round(Kc / (ms * 1e-3), 1),
+            "projections": "MXFP8 (E4M3, E8M0 scale per 32), peak 5.0 PFLOP/s dense fp8",
+            "kernels": kernels}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -206,6 +252,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-actions", action="store_true",
                     help="skip the per-action heads + utility top-K measurement")
+    ap.add_argument("--no-mxfp8", action="store_true",
+                    help="skip the fp8-projection variant's measurement")
     ap.add_argument("--flush-mall", action="store_true",
                     help="write a 512 MiB scratch buffer before every rank step (evicts the "
                          "256 MB MALL; for counter runs, not for the headline number)")
@@ -352,6 +400,10 @@ def main():
     glat = np.array(glat) if glat else np.array([np.nan])
 
     flops = path_flops(inp)
+
+    def pct(v, q):          # null when the pass was skipped (JSON has no NaN)
+        return None if np.all(np.isnan(v)) else round(float(np.nanpercentile(v, q)), 4)
+
     out = {
         "metric": "candidate scores/sec (1 GPU)",
         "value": round(Kc / (ms * 1e-3), 1),
@@ -369,18 +421,18 @@ def main():
         "step_ms": {"p10": round(float(np.percentile(per_step, 10)), 4),
                     "p50": round(float(np.percentile(per_step, 50)), 4),
                     "p90": round(float(np.percentile(per_step, 90)), 4)},
-        "user_latency_ms": {"p50": round(float(np.percentile(lat, 50)), 4),
-                            "p90": round(float(np.percentile(lat, 90)), 4),
-                            "calls": int(lat.size)},
-        "user_latency_graph_ms": {"p50": round(float(np.percentile(glat, 50)), 4),
-                                  "p90": round(float(np.percentile(glat, 90)), 4),
-                                  "replays": int(glat.size)},
+        "user_latency_ms": {"p50": pct(lat, 50), "p90": pct(lat, 90),
+                            "calls": int(np.sum(~np.isnan(lat)))},
+        "user_latency_graph_ms": {"p50": pct(glat, 50), "p90": pct(glat, 90),
+                                  "replays": int(np.sum(~np.isnan(glat)))},
         "encode_ms": round(encode_ms, 3),
         "roofline": roof,
         "kernels": kernels,
     }
     if not args.no_actions:
         out["actions_topk"] = actions_topk(args, inp, model, kv, hs, cs, C, Kc, ev, stream)
+    if not args.no_mxfp8 and inp.dtype == "bf16" and inp.d % 256 == 0 and inp.F % 128 == 0:
+        out["mxfp8"] = mxfp8_rank(args, inp, kv, hs, cs, C, Kc, ev, stream, work)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(inp)
     print(json.dumps(out), flush=True)

@@ -53,7 +53,7 @@ typedef enum {
     UPR_ERR_LIMIT = 9       /* an argument exceeds a documented limit          */
 } upr_status;
 
-typedef enum { UPR_F32 = 0, UPR_BF16 = 1 } upr_dtype;
+typedef enum { UPR_F32 = 0, UPR_BF16 = 1, UPR_BF16_MXFP8 = 2 } upr_dtype;
 
 /* Model shape.  Supported: head_dim in {32, 64}; d_model = n_heads*head_dim,
  * a multiple of 64 and at most 1024; d_ff a multiple of 64 and at most 8192;
@@ -68,6 +68,17 @@ typedef enum { UPR_F32 = 0, UPR_BF16 = 1 } upr_dtype;
  *             normalisation statistics, softmax and every accumulation are
  *             fp32.  Activations entering the projections must stay within
  *             the fp16 range (|x| < 65504).
+ *   UPR_BF16_MXFP8: the UPR_BF16 model (same weight blob, tokens and cache;
+ *             encode unchanged) whose ranking layers run their four
+ *             projections (Q/K/V, O, FFN up, FFN down) in FP8 (paper Sec. 3,
+ *             "FP8 quantization": E4M3 in the forward pass) with OCP
+ *             microscaling: every weight row and every projection input row
+ *             (LayerNorm outputs, attention output, FFN hidden) is encoded
+ *             as E4M3 values with one power-of-two E8M0 scale per 32
+ *             consecutive values along the contraction axis (see
+ *             upr_mx_quantize_host), and the products accumulate in fp32 on
+ *             gfx950's scaled fp8 matrix instructions.  Requires d_model a
+ *             multiple of 256 and d_ff a multiple of 128.
  * ln_eps is the LayerNorm epsilon. */
 typedef struct {
     int32_t d_model;
@@ -235,6 +246,44 @@ upr_status upr_rank_actions(const upr_model* model, const upr_heads* heads,
  * (UPR_ERR_LIMIT otherwise).  Allocates nothing. */
 upr_status upr_topk_by_utility(const float* utility, const upr_segments* cand, int32_t K,
                                int32_t* topk_rows, float* topk_utility, void* stream);
+
+/* ---- MXFP8 encoding (the UPR_BF16_MXFP8 projections' operand format) ----
+ * OCP microscaling with E4M3 elements: each row of x [rows, k] (k a positive
+ * multiple of 32) is cut into blocks of 32 consecutive values; a block with
+ * largest magnitude a gets e = floor(log2 a) - 8 (8 = exponent of E4M3's
+ * largest value, 448), at least -127 (-127 also for an all-zero block); its
+ * scale byte is e + 127 (E8M0) and each value v becomes the E4M3 code of
+ * v / 2^e rounded to the nearest E4M3 value, ties to even, magnitudes above
+ * 448 saturated to 448, negative values (also those rounding to zero)
+ * keeping the sign bit.  codes is [rows, k] bytes, scales [rows, k / 32]
+ * bytes, both row-major.  Input values must be finite. */
+
+/* Host encoding (host pointers, caller-owned).  UPR_ERR_NULL / UPR_ERR_LIMIT
+ * (k not a positive multiple of 32, rows < 0). */
+upr_status upr_mx_quantize_host(const float* x, int64_t rows, int32_t k, uint8_t* codes,
+                                uint8_t* scales);
+
+/* Input element type of upr_mx_quantize. */
+typedef enum { UPR_MX_IN_F32 = 0, UPR_MX_IN_F16 = 1, UPR_MX_IN_BF16 = 2 } upr_mx_input;
+
+/* Device encoding on `stream` (device pointers, caller-owned; x of element
+ * type in_type, a upr_mx_input value).  Fails (writing nothing) with
+ * UPR_ERR_NULL, UPR_ERR_DTYPE or UPR_ERR_LIMIT as the host call.  Allocates
+ * nothing. */
+upr_status upr_mx_quantize(const void* x, int32_t in_type, int64_t rows, int32_t k,
+                           uint8_t* codes, uint8_t* scales, void* stream);
+
+/* out[M, N] += A W^T + bias on the scaled fp8 matrix instructions, A
+ * [M, K] and W [N, K] MXFP8 encodings (codes and scales as above, device
+ * memory), bias [N] and out [M, N] fp32 (device, row-major, out updated in
+ * place).  This is the projection the UPR_BF16_MXFP8 ranking layers run,
+ * exposed for testing and for callers with pre-encoded operands.  K a
+ * positive multiple of 128, N a positive multiple of 8, M >= 0
+ * (UPR_ERR_LIMIT otherwise); NULL pointers give UPR_ERR_NULL.  Allocates
+ * nothing. */
+upr_status upr_mx_linear(const uint8_t* a_codes, const uint8_t* a_scales, const uint8_t* w_codes,
+                         const uint8_t* w_scales, const float* bias, int64_t M, int32_t N,
+                         int32_t K, float* out, void* stream);
 
 /* Diagnostics: per-kernel timing with HIP events.  While enabled, encode and
  * rank record a pair of hipEvents on the call's stream around every kernel

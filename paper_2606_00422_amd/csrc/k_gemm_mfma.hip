@@ -29,7 +29,21 @@
 // Tile order is XCD-aware: workgroup b runs on XCD b % 8 and the tiles are
 // renumbered so each XCD sweeps a contiguous range of (M-panel, N-tile)
 // pairs; the N-tiles of one A row-panel then share one L2.
+//
+// MXFP8 operands (fp8 projection variant).  The same kernel with E4M3 codes:
+// a 128-byte LDS row now holds 128 K-values, so one K-step covers twice the
+// depth with the same loads, swizzle and LDS traffic, and the MFMA is
+// v_mfma_scale_f32_32x32x64_f8f6f4 (twice the fp16 rate).  Its operand
+// layout (probed): lane l holds row l % 32; the 32 bytes of lane l are K
+// [16h, 16h+16) and [32+16h, 32+16h+16) of the instruction's 64 (h = l / 32),
+// and the E8M0 scale lane l supplies applies to 32-value block h of its row
+// (bytes 0-15 of lanes l and l+32 form block 0).  So a lane reads LDS chunks
+// 4kk + h and 4kk + 2 + h, and takes byte 2kk + h of its row's scale dword
+// (the four blocks of the K-step; op_sel picks byte 2kk after a shift by
+// 8h).  The scale dwords of a K-step (one per row of A and of W) ride along
+// with the tile loads into two small LDS arrays per stage.
 #include "epilogue.h"
+#include "mx.h"
 #include "upr_plan.h"
 
 namespace upr {
@@ -40,6 +54,8 @@ typedef __attribute__((ext_vector_type(8))) _Float16 h8;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((ext_vector_type(4))) unsigned u32x4;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(8))) int i32x8;
+typedef __attribute__((ext_vector_type(4))) int i32x4;
 
 constexpr int kBM = 256, kBN = 256, kBK = 64;     // block tile
 constexpr int kThreads = 512;                      // 8 waves
@@ -164,6 +180,63 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
             __builtin_amdgcn_s_waitcnt(0xC07F);
             __builtin_amdgcn_wave_barrier();
         }
+    } else if constexpr (MODE == EPI_GELU_MX) {
+        // In the MFMA layout a lane holds, for row 32i + lane%32, sixteen of
+        // the 32 columns of block j (8q + 4h .. +3, q = 0..3) and lane l^32
+        // the other sixteen: one exchange gives the block maximum.  After
+        // encoding, two v_permlane32_swap exchanges give lane l (h = 0) the
+        // codes of columns 0-15 and lane l+32 those of 16-31, so each writes
+        // 16 consecutive bytes; lanes of h = 0 write the row's two scale bytes.
+        float4 bq[kTN][4];
+#pragma unroll
+        for (int j = 0; j < kTN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int col = wcol0 + j * 32 + 8 * q + 4 * lhalf;
+                bq[j][q] = col < N ? *reinterpret_cast<const float4*>(epi.bias + col)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+        uint8_t* const codes = static_cast<uint8_t*>(epi.out);
+        uint8_t* const scales = static_cast<uint8_t*>(epi.out_scales);
+        const int64_t lds = epi.ldo / kMxBlock;
+        const bool cols_ok = wcol0 < N;                 // N is a multiple of 64
+#pragma unroll
+        for (int i = 0; i < kTM; ++i) {
+            const int64_t row = wrow0 + i * 32 + lrow;
+            unsigned sc2 = 0;
+#pragma unroll
+            for (int j = 0; j < kTN; ++j) {
+                float v[16];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    v[4 * q + 0] = gelu_fast(fmaf(acc[j][i][4 * q + 0], sc, bq[j][q].x));
+                    v[4 * q + 1] = gelu_fast(fmaf(acc[j][i][4 * q + 1], sc, bq[j][q].y));
+                    v[4 * q + 2] = gelu_fast(fmaf(acc[j][i][4 * q + 2], sc, bq[j][q].z));
+                    v[4 * q + 3] = gelu_fast(fmaf(acc[j][i][4 * q + 3], sc, bq[j][q].w));
+                }
+                float amax = 0.f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) amax = fmaxf(amax, fabsf(v[r]));
+                amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
+                const int e = mx_block_exp(amax);
+                const float inv = mx_inv_scale(e);
+                unsigned u[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    u[q] = mx_pack4(v[4 * q] * inv, v[4 * q + 1] * inv, v[4 * q + 2] * inv,
+                                    v[4 * q + 3] * inv);
+                const auto r02 = __builtin_amdgcn_permlane32_swap(u[0], u[2], false, false);
+                const auto r13 = __builtin_amdgcn_permlane32_swap(u[1], u[3], false, false);
+                const u32x4 o = {r02[0], r02[1], r13[0], r13[1]};
+                sc2 |= (unsigned)(e + 127) << (8 * j);
+                if (row < M && cols_ok)
+                    __builtin_nontemporal_store(
+                        o, reinterpret_cast<u32x4*>(codes + row * epi.ldo + wcol0 + j * 32 + 16 * lhalf));
+            }
+            if (lhalf == 0 && row < M && cols_ok)
+                *reinterpret_cast<unsigned short*>(scales + row * lds + wcol0 / kMxBlock) =
+                    (unsigned short)sc2;
+        }
     } else {
         float4 bq[kTN][4];
 #pragma unroll
@@ -250,18 +323,26 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
     }
 }
 
-template <int MODE>
-__global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict__ A, int64_t lda,
-                                                           const f16* __restrict__ W, int64_t M,
-                                                           int N, int K, Epilogue epi) {
+template <int MODE, bool MX>
+__global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restrict__ Av, int64_t lda,
+                                                           const void* __restrict__ Wv,
+                                                           const uint8_t* __restrict__ As,
+                                                           const uint8_t* __restrict__ Ws,
+                                                           int64_t M, int N, int K, Epilogue epi) {
     // Two LDS stages as separate arrays: the compiler can then tell that
     // fragment reads of one stage do not alias the loads filling the other.
     __shared__ __attribute__((aligned(16))) f16 sA0[kBM * kBK];
     __shared__ __attribute__((aligned(16))) f16 sA1[kBM * kBK];
     __shared__ __attribute__((aligned(16))) f16 sB0[kBN * kBK];
     __shared__ __attribute__((aligned(16))) f16 sB1[kBN * kBK];
+    // MXFP8: the K-step's scale dword of every row of A and of W
+    __shared__ uint32_t sSA0[kBM], sSA1[kBM], sSB0[kBN], sSB1[kBN];
+    constexpr int kEB = MX ? 1 : 2;         // bytes per operand value
+    const char* const A = static_cast<const char*>(Av);
+    const char* const W = static_cast<const char*>(Wv);
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);     // uniform: wave-derived values stay scalar
     const int wm = wave / kWavesN, wn = wave % kWavesN;
     const int tiles_n = (N + kBN - 1) / kBN;
     const int t = xcd_tile(blockIdx.x, gridDim.x);
@@ -274,9 +355,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict
     const int64_t rows_a = M - m0 < kBM ? M - m0 : kBM;
     const int rows_b = N - n0 < kBN ? N - n0 : kBN;
     const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(A + m0 * lda), (short)0, (int)(rows_a * lda * 2), 0x00020000);
+        (void*)(A + m0 * lda * kEB), (short)0, (int)(rows_a * lda * kEB), 0x00020000);
     const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(W + (int64_t)n0 * K), (short)0, (int)((int64_t)rows_b * K * 2), 0x00020000);
+        (void*)(W + (int64_t)n0 * K * kEB), (short)0, (int)((int64_t)rows_b * K * kEB), 0x00020000);
 
     // Direct global -> LDS loads by the leading waves: a load instruction's
     // 64 lanes fill 64 consecutive 16-byte LDS slots = 8 rows.  Load i of
@@ -291,10 +372,28 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
         const int lch = (lane & 7) ^ ((p * 4 + (lane >> 4)) & 7);
-        voA[p] = (int)(((lw * kLoadsA + p) * 8 + (lane >> 3)) * lda * 2 + lch * 16);
-        voB[p] = ((lw * kLoadsB + p) * 8 + (lane >> 3)) * K * 2 + lch * 16;
+        voA[p] = (int)(((lw * kLoadsA + p) * 8 + (lane >> 3)) * lda * kEB + lch * 16);
+        voB[p] = ((lw * kLoadsB + p) * 8 + (lane >> 3)) * K * kEB + lch * 16;
     }
-    const int rowstepA = (int)(16 * lda * 2), rowstepB = 16 * K * 2;
+    const int rowstepA = (int)(16 * lda * kEB), rowstepB = 16 * K * kEB;
+    // MXFP8 scales: leading wave lw loads the dwords of rows 64 lw .. +63 of
+    // A and of W for a K-step (K/32 bytes per row; dword t = blocks 4t..4t+3)
+    const int kblk = K / kMxBlock;
+    const __amdgpu_buffer_rsrc_t rsSA = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(MX ? As + m0 * kblk : As), (short)0, MX ? (int)(rows_a * kblk) : 0, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rsSB = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(MX ? Ws + (int64_t)n0 * kblk : Ws), (short)0, MX ? (int)((int64_t)rows_b * kblk) : 0,
+        0x00020000);
+    const int voS = (lw * 64 + lane) * kblk;
+    auto issue_scales = [&](uint32_t* dSA, uint32_t* dSB, int t) {
+        if constexpr (MX) {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rsSA, (__attribute__((address_space(3))) void*)(dSA + lw * 64), 4, voS + 4 * t, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rsSB, (__attribute__((address_space(3))) void*)(dSB + lw * 64), 4, voS + 4 * t, 0, 0, 0);
+        }
+    };
+    // k0: byte offset of the K-step within a row (128 per step)
     auto issue_loads = [&](f16* dA, f16* dB, int k0) {
         // opaque copies keep the per-load offsets from being hoisted into
         // sixteen live registers
@@ -304,12 +403,12 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict
         for (int i = 0; i < kLoadsA; ++i)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
                 rsA, (__attribute__((address_space(3))) void*)(dA + (lw * kLoadsA + i) * 64 * 8),
-                16, voA[i & 1] + (i >> 1) * rsa + k0 * 2, 0, 0, 0);
+                16, voA[i & 1] + (i >> 1) * rsa + k0, 0, 0, 0);
 #pragma unroll
         for (int i = 0; i < kLoadsB; ++i)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
                 rsB, (__attribute__((address_space(3))) void*)(dB + (lw * kLoadsB + i) * 64 * 8),
-                16, voB[i & 1] + (i >> 1) * rsb + k0 * 2, 0, 0, 0);
+                16, voB[i & 1] + (i >> 1) * rsb + k0, 0, 0, 0);
     };
 
     f32x16 acc[kTN][kTM];
@@ -321,28 +420,86 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict
             for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
 
     const int lrow = lane & 31, lhalf = lane >> 5;
+    // fp16: 16-deep fragments; MXFP8: 64-deep fragments + scale dwords.  Each
+    // wave reads all of a K-step's fragments in its read phase: the leading
+    // waves refill a stage as soon as the trailing waves' read phase on it
+    // has ended.
     h8 a[kBK / 16][kTM], b[kBK / 16][kTN];
-    auto read_frags = [&](const f16* cA, const f16* cB) {
+    i32x8 am[2][kTM], bm[2][kTN];
+    unsigned sa[kTM], sb[kTN];
+    // Byte offsets, within a stage, of this lane's first fragment row at
+    // logical chunk 2m + lhalf (swz written out: the key (row / 2) % 8 is the
+    // same for every row tile of the lane).  Row tiles add constants, which
+    // fold into the read instructions.
+    int offA[4], offB[4];
 #pragma unroll
-        for (int kk = 0; kk < kBK / 16; ++kk) {
-            const int ch = kk * 2 + lhalf;
+    for (int m = 0; m < 4; ++m) {
+        const int ch = (((2 * m + lhalf) ^ ((lrow >> 1) & 7)) << 4);
+        offA[m] = (wm * kWM + lrow) * (kBK * 2) + ch;
+        offB[m] = (wn * kWN + lrow) * (kBK * 2) + ch;
+    }
+    // t-th row tile (32 rows down), K-half kk
+    auto frag_mx = [&](const f16* c, const int (&off)[4], int t, int kk) {
+        const char* p = reinterpret_cast<const char*>(c) + t * 32 * (kBK * 2);
+        i32x8 f;
+        f.lo = *reinterpret_cast<const i32x4*>(p + off[2 * kk]);
+        f.hi = *reinterpret_cast<const i32x4*>(p + off[2 * kk + 1]);
+        return f;
+    };
+    auto read_frags = [&](const f16* cA, const f16* cB, const uint32_t* cSA, const uint32_t* cSB) {
+        if constexpr (MX) {
+            // recomputed addresses per step (not hoisted into 24 registers)
+            asm volatile("" : "+v"(offA[0]), "+v"(offA[1]), "+v"(offA[2]), "+v"(offA[3]),
+                         "+v"(offB[0]), "+v"(offB[1]), "+v"(offB[2]), "+v"(offB[3]));
 #pragma unroll
-            for (int i = 0; i < kTM; ++i)
-                a[kk][i] = *reinterpret_cast<const h8*>(&cA[swz(wm * kWM + i * 32 + lrow, ch)]);
+            for (int kk = 0; kk < 2; ++kk) {
 #pragma unroll
-            for (int j = 0; j < kTN; ++j)
-                b[kk][j] = *reinterpret_cast<const h8*>(&cB[swz(wn * kWN + j * 32 + lrow, ch)]);
+                for (int i = 0; i < kTM; ++i) am[kk][i] = frag_mx(cA, offA, i, kk);
+#pragma unroll
+                for (int j = 0; j < kTN; ++j) bm[kk][j] = frag_mx(cB, offB, j, kk);
+            }
+#pragma unroll
+            for (int i = 0; i < kTM; ++i) sa[i] = cSA[wm * kWM + i * 32 + lrow] >> (8 * lhalf);
+#pragma unroll
+            for (int j = 0; j < kTN; ++j) sb[j] = cSB[wn * kWN + j * 32 + lrow] >> (8 * lhalf);
+        } else {
+#pragma unroll
+            for (int kk = 0; kk < kBK / 16; ++kk) {
+                const int ch = kk * 2 + lhalf;
+#pragma unroll
+                for (int i = 0; i < kTM; ++i)
+                    a[kk][i] = *reinterpret_cast<const h8*>(&cA[swz(wm * kWM + i * 32 + lrow, ch)]);
+#pragma unroll
+                for (int j = 0; j < kTN; ++j)
+                    b[kk][j] = *reinterpret_cast<const h8*>(&cB[swz(wn * kWN + j * 32 + lrow, ch)]);
+            }
         }
     };
     auto compute = [&]() {
-#pragma unroll
-        for (int kk = 0; kk < kBK / 16; ++kk)
+        if constexpr (MX) {
+            // op_sel picks byte 2kk of the (per-lane shifted) scale dwords
 #pragma unroll
             for (int j = 0; j < kTN; ++j)
 #pragma unroll
                 for (int i = 0; i < kTM; ++i)
-                    acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(b[kk][j], a[kk][i],
-                                                                       acc[j][i], 0, 0, 0);
+                    acc[j][i] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                        bm[0][j], am[0][i], acc[j][i], 0, 0, 0, (int)sb[j], 0, (int)sa[i]);
+#pragma unroll
+            for (int j = 0; j < kTN; ++j)
+#pragma unroll
+                for (int i = 0; i < kTM; ++i)
+                    acc[j][i] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                        bm[1][j], am[1][i], acc[j][i], 0, 0, 2, (int)sb[j], 2, (int)sa[i]);
+        } else {
+#pragma unroll
+            for (int kk = 0; kk < kBK / 16; ++kk)
+#pragma unroll
+                for (int j = 0; j < kTN; ++j)
+#pragma unroll
+                    for (int i = 0; i < kTM; ++i)
+                        acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(b[kk][j], a[kk][i],
+                                                                           acc[j][i], 0, 0, 0);
+        }
     };
 
     // Every wave runs the same read / MFMA sequence; the trailing waves run
@@ -351,10 +508,14 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict
     // issue step t+1's loads at the start of their step t into the other
     // stage (last read by the trailing waves in the phase just ended) and
     // wait for them at the end of step t, before anyone reads them.
-    const int nk = K / kBK;
-    auto kstep = [&](const f16* cA, const f16* cB, f16* nA, f16* nB, int t) {
-        if (lead && t + 1 < nk) issue_loads(nA, nB, (t + 1) * kBK);
-        read_frags(cA, cB);
+    const int nk = K / (kBK * 2 / kEB);
+    auto kstep = [&](const f16* cA, const f16* cB, const uint32_t* cSA, const uint32_t* cSB,
+                     f16* nA, f16* nB, uint32_t* nSA, uint32_t* nSB, int t) {
+        if (lead && t + 1 < nk) {
+            issue_loads(nA, nB, (t + 1) * kBK * 2);
+            issue_scales(nSA, nSB, t + 1);
+        }
+        read_frags(cA, cB, cSA, cSB);
         __builtin_amdgcn_s_waitcnt(0xC07F);     // lgkmcnt(0): fragments in registers
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_sched_barrier(0);
@@ -365,16 +526,19 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict
         __builtin_amdgcn_sched_barrier(0);
     };
 
-    if (lead) issue_loads(sA0, sB0, 0);
+    if (lead) {
+        issue_loads(sA0, sB0, 0);
+        issue_scales(sSA0, sSB0, 0);
+    }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (!lead) __builtin_amdgcn_s_barrier();
     int kt = 0;
     for (; kt + 2 <= nk; kt += 2) {
-        kstep(sA0, sB0, sA1, sB1, kt);
-        kstep(sA1, sB1, sA0, sB0, kt + 1);
+        kstep(sA0, sB0, sSA0, sSB0, sA1, sB1, sSA1, sSB1, kt);
+        kstep(sA1, sB1, sSA1, sSB1, sA0, sB0, sSA0, sSB0, kt + 1);
     }
-    if (kt < nk) kstep(sA0, sB0, sA1, sB1, kt);
+    if (kt < nk) kstep(sA0, sB0, sSA0, sSB0, sA1, sB1, sSA1, sSB1, kt);
     // Past here every wave has finished its fragment reads (the trailing
     // waves' last reads precede the barrier that ended the leading waves'
     // last step), so the stages are free for the epilogue; the leading
@@ -390,11 +554,12 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const f16* __restrict
     if (lead) __builtin_amdgcn_s_barrier();
 }
 
-template <int MODE>
-hipError_t launch_mode(const f16* A, int64_t lda, const f16* W, int64_t M, int N, int K,
-                       const Epilogue& epi, hipStream_t s) {
+template <int MODE, bool MX>
+hipError_t launch_mode(const void* A, int64_t lda, const void* W, const uint8_t* As,
+                       const uint8_t* Ws, int64_t M, int N, int K, const Epilogue& epi,
+                       hipStream_t s) {
     const int64_t tiles = ((M + kBM - 1) / kBM) * (int64_t)((N + kBN - 1) / kBN);
-    k_gemm_mfma<MODE><<<(unsigned)tiles, kThreads, 0, s>>>(A, lda, W, M, N, K, epi);
+    k_gemm_mfma<MODE, MX><<<(unsigned)tiles, kThreads, 0, s>>>(A, lda, W, As, Ws, M, N, K, epi);
     return hipGetLastError();
 }
 
@@ -409,17 +574,38 @@ hipError_t launch_gemm_mfma(const f16* A, int64_t lda, const f16* W, int64_t M, 
     switch (epi.mode) {
         case EPI_STORE:
             if (epi.ldo % 8 != 0 || epi.scale_cols % 4 != 0) return hipErrorInvalidValue;
-            return launch_mode<EPI_STORE>(A, lda, W, M, N, K, epi, s);
+            return launch_mode<EPI_STORE, false>(A, lda, W, nullptr, nullptr, M, N, K, epi, s);
         case EPI_GELU:
             if (epi.ldo % 8 != 0) return hipErrorInvalidValue;
-            return launch_mode<EPI_GELU>(A, lda, W, M, N, K, epi, s);
+            return launch_mode<EPI_GELU, false>(A, lda, W, nullptr, nullptr, M, N, K, epi, s);
         case EPI_RESID:
             if (epi.ldr % 4 != 0) return hipErrorInvalidValue;
-            return launch_mode<EPI_RESID>(A, lda, W, M, N, K, epi, s);
+            return launch_mode<EPI_RESID, false>(A, lda, W, nullptr, nullptr, M, N, K, epi, s);
         case EPI_QKV_CACHE:
             if (epi.ldo % 8 != 0 || epi.head_dim % 8 != 0 || epi.d_model % 8 != 0)
                 return hipErrorInvalidValue;
-            return launch_mode<EPI_QKV_CACHE>(A, lda, W, M, N, K, epi, s);
+            return launch_mode<EPI_QKV_CACHE, false>(A, lda, W, nullptr, nullptr, M, N, K, epi, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_gemm_mx(const uint8_t* A, const uint8_t* A_scales, const uint8_t* W,
+                          const uint8_t* W_scales, int64_t M, int N, int K, const Epilogue& epi,
+                          hipStream_t s) {
+    using namespace gemm_detail;
+    if (M == 0) return hipSuccess;
+    // whole 128-deep K-steps over rows of K codes, 16-byte output chunks
+    if (K <= 0 || K % 128 != 0 || N % 8 != 0 || !A_scales || !W_scales) return hipErrorInvalidValue;
+    switch (epi.mode) {
+        case EPI_STORE:
+            if (epi.ldo % 8 != 0 || epi.scale_cols % 4 != 0) return hipErrorInvalidValue;
+            return launch_mode<EPI_STORE, true>(A, K, W, A_scales, W_scales, M, N, K, epi, s);
+        case EPI_RESID:
+            if (epi.ldr % 4 != 0) return hipErrorInvalidValue;
+            return launch_mode<EPI_RESID, true>(A, K, W, A_scales, W_scales, M, N, K, epi, s);
+        case EPI_GELU_MX:
+            if (N % 64 != 0 || epi.ldo % 64 != 0 || !epi.out_scales) return hipErrorInvalidValue;
+            return launch_mode<EPI_GELU_MX, true>(A, K, W, A_scales, W_scales, M, N, K, epi, s);
         default: return hipErrorInvalidValue;
     }
 }

@@ -5,6 +5,7 @@
 // (16-byte loads, 8-byte half stores); otherwise features lane + 64 i.
 // Statistics are two-pass in fp32 over the registers: mean, then the mean
 // of squared deviations (population variance), as LayerNorm defines them.
+#include "mx.h"
 #include "upr_internal.h"
 
 namespace upr {
@@ -94,6 +95,38 @@ __device__ __forceinline__ void store_normed(TA* __restrict__ out, const float (
     }
 }
 
+// Writes LN(v) for the row as MXFP8 (fp8 projection inputs): the VEC layout
+// gives a lane four consecutive features per 256-feature group, so one
+// 32-feature block is eight consecutive lanes; codes[c] is feature c's E4M3
+// code, scales[c / 32] its block's E8M0 byte.
+__device__ __forceinline__ void store_normed_mx(uint8_t* __restrict__ codes,
+                                                uint8_t* __restrict__ scales,
+                                                const float (&v)[kMaxPerLane], int d, int lane,
+                                                float mu, float rstd,
+                                                const float* __restrict__ gain,
+                                                const float* __restrict__ shift) {
+    const int per = d >> 6;
+#pragma unroll
+    for (int j = 0; j < kMaxPerLane / 4; ++j)
+        if (4 * j < per) {
+            const int c = j * 256 + 4 * lane;
+            const float4 gq = *reinterpret_cast<const float4*>(gain + c);
+            const float4 bq = *reinterpret_cast<const float4*>(shift + c);
+            const float y0 = keep_f32(fmaf((v[4 * j] - mu) * rstd, gq.x, bq.x));
+            const float y1 = keep_f32(fmaf((v[4 * j + 1] - mu) * rstd, gq.y, bq.y));
+            const float y2 = keep_f32(fmaf((v[4 * j + 2] - mu) * rstd, gq.z, bq.z));
+            const float y3 = keep_f32(fmaf((v[4 * j + 3] - mu) * rstd, gq.w, bq.w));
+            float amax = fmaxf(fmaxf(fabsf(y0), fabsf(y1)), fmaxf(fabsf(y2), fabsf(y3)));
+            amax = fmaxf(amax, __shfl_xor(amax, 1, 64));
+            amax = fmaxf(amax, __shfl_xor(amax, 2, 64));
+            amax = fmaxf(amax, __shfl_xor(amax, 4, 64));
+            const int e = mx_block_exp(amax);
+            const float inv = mx_inv_scale(e);
+            *reinterpret_cast<uint32_t*>(codes + c) = mx_pack4(y0 * inv, y1 * inv, y2 * inv, y3 * inv);
+            if ((lane & 7) == 0) scales[c >> 5] = (uint8_t)(e + 127);
+        }
+}
+
 // g = float(x); a = LN(g)  (residual stream initialisation fused with the
 // first layer's LayerNorm).
 template <bool VEC, typename TKV, typename TA>
@@ -143,6 +176,40 @@ __global__ __launch_bounds__(256) void k_layernorm(const float* __restrict__ g, 
     load_row<VEC>(g + row * d, d, lane, v);
     row_stats(v, d, eps, mu, rstd);
     store_normed<VEC>(a + row * d, v, d, lane, mu, rstd, gain, shift);
+}
+
+// MXFP8 LayerNorm outputs (d a multiple of 256).  INIT: the residual stream
+// starts here, g = float(x).
+template <bool INIT, typename TKV>
+__global__ __launch_bounds__(256) void k_layernorm_mx(const TKV* __restrict__ x,
+                                                      float* __restrict__ g,
+                                                      uint8_t* __restrict__ codes,
+                                                      uint8_t* __restrict__ scales, int64_t rows,
+                                                      int d, const float* __restrict__ gain,
+                                                      const float* __restrict__ shift, float eps) {
+    const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (row >= rows) return;
+    const int per = d >> 6;
+    float v[kMaxPerLane], mu, rstd;
+    if constexpr (INIT) {
+        const TKV* xr = x + row * d;
+        float* gr = g + row * d;
+#pragma unroll
+        for (int j = 0; j < kMaxPerLane / 4; ++j)
+            if (4 * j < per) {
+                const int c = j * 256 + 4 * lane;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) v[4 * j + t] = to_f(xr[c + t]);
+                *reinterpret_cast<float4*>(gr + c) =
+                    make_float4(v[4 * j], v[4 * j + 1], v[4 * j + 2], v[4 * j + 3]);
+            }
+    } else {
+        load_row<true>(g + row * d, d, lane, v);
+    }
+    row_stats(v, d, eps, mu, rstd);
+    store_normed_mx(codes + row * d, scales + row * (d / kMxBlock), v, d, lane, mu, rstd, gain,
+                    shift);
 }
 
 template <bool VEC>
@@ -215,6 +282,28 @@ hipError_t launch_layernorm(const float* g, TA* a, int64_t rows, int d, const fl
     return hipGetLastError();
 }
 
+template <typename TKV>
+hipError_t launch_init_layernorm_mx(const TKV* x, float* g, uint8_t* codes, uint8_t* scales,
+                                    int64_t rows, int d, const float* gain, const float* shift,
+                                    float eps, hipStream_t s) {
+    if (rows == 0) return hipSuccess;
+    if (d % 256 != 0) return hipErrorInvalidValue;
+    k_layernorm_mx<true, TKV><<<grid_rows(rows), 256, 0, s>>>(x, g, codes, scales, rows, d, gain,
+                                                             shift, eps);
+    return hipGetLastError();
+}
+
+hipError_t launch_layernorm_mx(const float* g, uint8_t* codes, uint8_t* scales, int64_t rows,
+                               int d, const float* gain, const float* shift, float eps,
+                               hipStream_t s) {
+    if (rows == 0) return hipSuccess;
+    if (d % 256 != 0) return hipErrorInvalidValue;
+    k_layernorm_mx<false, float><<<grid_rows(rows), 256, 0, s>>>(nullptr, const_cast<float*>(g),
+                                                                codes, scales, rows, d, gain,
+                                                                shift, eps);
+    return hipGetLastError();
+}
+
 hipError_t launch_score_head(const float* g, float* scores, int64_t rows, int d,
                              const FinalWeights& fw, float eps, hipStream_t s) {
     if (rows == 0) return hipSuccess;
@@ -233,6 +322,9 @@ template hipError_t launch_init_layernorm<float, float>(const float*, float*, fl
 template hipError_t launch_init_layernorm<bf16, f16>(const bf16*, float*, f16*, int64_t, int,
                                                      const float*, const float*, float,
                                                      hipStream_t);
+template hipError_t launch_init_layernorm_mx<bf16>(const bf16*, float*, uint8_t*, uint8_t*,
+                                                   int64_t, int, const float*, const float*,
+                                                   float, hipStream_t);
 template hipError_t launch_layernorm<float>(const float*, float*, int64_t, int, const float*,
                                             const float*, float, hipStream_t);
 template hipError_t launch_layernorm<f16>(const float*, f16*, int64_t, int, const float*,

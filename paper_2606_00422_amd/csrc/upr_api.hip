@@ -55,10 +55,16 @@ upr_status ok() {
     return UPR_OK;
 }
 
+// bf16 storage (tokens, cache): UPR_BF16 and its fp8-projection variant
+bool bf16_family(int32_t dt) { return dt == UPR_BF16 || dt == UPR_BF16_MXFP8; }
+
 upr_status check_config(const upr_config* c) {
     if (!c) return fail(UPR_ERR_NULL, "config is NULL");
-    if (c->dtype != UPR_F32 && c->dtype != UPR_BF16)
-        return fail(UPR_ERR_DTYPE, "dtype %d is neither UPR_F32 nor UPR_BF16", c->dtype);
+    if (c->dtype != UPR_F32 && !bf16_family(c->dtype))
+        return fail(UPR_ERR_DTYPE, "dtype %d is not UPR_F32, UPR_BF16 or UPR_BF16_MXFP8", c->dtype);
+    if (c->dtype == UPR_BF16_MXFP8 && (c->d_model % 256 != 0 || c->d_ff % 128 != 0))
+        return fail(UPR_ERR_CONFIG, "UPR_BF16_MXFP8 needs d_model %% 256 == 0 and d_ff %% 128 == 0 "
+                    "(got %d, %d)", c->d_model, c->d_ff);
     if (c->head_dim != 32 && c->head_dim != 64)
         return fail(UPR_ERR_CONFIG, "head_dim %d not supported (32 or 64)", c->head_dim);
     if (c->n_heads <= 0 || (int64_t)c->n_heads * c->head_dim != c->d_model)
@@ -125,11 +131,12 @@ struct ImageBuilder {
     upr_dtype dtype;
     static size_t align(size_t x) { return (x + 255) & ~size_t(255); }
     size_t add_mat(const float* src, int64_t n, float* scale) {
-        const size_t es = dtype == UPR_BF16 ? 2 : 4;
+        const bool bf = bf16_family(dtype);
+        const size_t es = bf ? 2 : 4;
         size_t off = align(img.size());
         img.resize(off + n * es);
         *scale = 1.0f;
-        if (dtype == UPR_BF16) {
+        if (bf) {
             float maxabs = 0.f;
             for (int64_t i = 0; i < n; ++i)
                 maxabs = std::fmax(maxabs, std::fabs(bf16_value(f32_to_bf16_rne(src[i]))));
@@ -154,6 +161,17 @@ struct ImageBuilder {
         img.resize(off + n * 4);
         std::memcpy(img.data() + off, src, n * 4);
         return off;
+    }
+    // MXFP8 encoding of a [rows, k] matrix, its values first rounded to bf16
+    // (the model's weights): codes at *codes_off, scales at *scales_off.
+    void add_mx(const float* src, int64_t rows, int k, size_t* codes_off, size_t* scales_off) {
+        std::vector<float> w(src, src + rows * k);
+        for (float& v : w) v = bf16_value(f32_to_bf16_rne(v));
+        *codes_off = align(img.size());
+        *scales_off = align(*codes_off + rows * k);
+        img.resize(*scales_off + rows * (k / 32));
+        upr::mx_quantize_host(w.data(), rows, k, reinterpret_cast<uint8_t*>(img.data() + *codes_off),
+                              reinterpret_cast<uint8_t*>(img.data() + *scales_off));
     }
     // Copies the image to new device memory (*dev) or fails.
     upr_status upload(void** dev) {
@@ -195,7 +213,7 @@ upr_status check_workspace(void* ws, size_t ws_bytes, size_t need) {
         UPR_HIP(__VA_ARGS__);                                                                   \
     } while (0)
 
-size_t elem_size(const upr_config& c) { return c.dtype == UPR_BF16 ? 2 : 4; }
+size_t elem_size(const upr_config& c) { return bf16_family(c.dtype) ? 2 : 4; }
 
 void* plane_ptr(const upr_config& c, const upr_kv_cache* cache, int layer, int kv) {
     const size_t off = (size_t)(layer * 2 + kv) * c.n_heads * cache->capacity_rows * c.head_dim;
@@ -208,6 +226,121 @@ void* plane_ptr(const upr_config& c, const upr_kv_cache* cache, int layer, int k
 // Encode / rank sequences
 // ---------------------------------------------------------------------------
 namespace upr {
+
+// ---- MXFP8 on the host
+
+// E4M3 code of s (finite): nearest value, ties to even (nearbyint in the
+// default rounding mode), magnitudes above 448 saturated, the sign bit kept
+// for negative values that round to zero.  Scaling by powers of two is exact.
+static uint8_t e4m3_code(float s) {
+    const uint8_t sign = std::signbit(s) ? 0x80 : 0x00;
+    const float a = std::fabs(s);
+    if (a >= 448.0f) return sign | 0x7E;
+    if (a < 0.015625f)                                 // below 2^-6: steps of 2^-9,
+        return sign | (uint8_t)std::nearbyint(a * 512.0f);   // 8 is the code of 2^-6
+    int ex;
+    std::frexp(a, &ex);                                // a in [2^(ex-1), 2^ex)
+    int e = ex - 1;                                    // in [-6, 8]
+    int m = (int)std::nearbyint(std::ldexp(a, 3 - e)); // in [8, 16]
+    if (m == 16) {
+        e += 1;
+        m = 8;
+    }
+    return sign | (uint8_t)(((e + 7) << 3) | (m - 8));
+}
+
+void mx_quantize_host(const float* x, int64_t rows, int k, uint8_t* codes, uint8_t* scales) {
+    for (int64_t r = 0; r < rows; ++r)
+        for (int b = 0; b < k / 32; ++b) {
+            const float* v = x + r * k + b * 32;
+            float amax = 0.f;
+            for (int i = 0; i < 32; ++i) amax = std::fmax(amax, std::fabs(v[i]));
+            int e = -127;
+            if (amax >= 0x1p-126f) {                    // normal: floor(log2 amax) = ex - 1
+                int ex;
+                std::frexp(amax, &ex);
+                e = std::max(ex - 1 - 8, -127);
+            }
+            scales[r * (k / 32) + b] = (uint8_t)(e + 127);
+            for (int i = 0; i < 32; ++i) codes[r * k + b * 32 + i] = e4m3_code(std::ldexp(v[i], -e));
+        }
+}
+
+// Candidate layers of the fp8-projection variant: the bf16 sequence with
+// MXFP8 projection operands (LayerNorms write MXFP8 directly, the attention
+// output is encoded from fp16, the FFN-up GEMM writes its GELU output as
+// MXFP8).
+static upr_status rank_layers_mx(const upr_model* m, const upr_kv_cache* cache,
+                                 const upr_segments* hist, const bf16* cand_emb,
+                                 const upr_segments* cand, const RankPlan& p, char* ws,
+                                 hipStream_t s) {
+    const upr_config& c = m->cfg;
+    const int d = c.d_model, F = c.d_ff, H = c.n_heads, D = c.head_dim;
+    const int64_t R = p.rows;
+    float* g = reinterpret_cast<float*>(ws + p.off_g);
+    uint8_t* ac = reinterpret_cast<uint8_t*>(ws + p.off_a);
+    uint8_t* asc = ac + align256((size_t)R * d);
+    bf16* qkv = reinterpret_cast<bf16*>(ws + p.off_qkv);
+    f16* o = reinterpret_cast<f16*>(ws + p.off_o);
+    uint8_t* hc = reinterpret_cast<uint8_t*>(ws + p.off_h);
+    uint8_t* hsc = hc + align256((size_t)R * F);
+    const float qscale = 1.4426950408889634f / std::sqrt((float)D);
+    UPR_LAUNCH("rank.init_ln1",
+               launch_init_layernorm_mx<bf16>(cand_emb + p.row0 * d, g, ac, asc, R, d,
+                                              m->layers[0].ln1_g, m->layers[0].ln1_b, c.ln_eps, s));
+    if (p.use_mfma_attn)
+        UPR_LAUNCH("rank.worklist",
+                   launch_attn_worklist(cand->offsets_dev, hist->offsets_dev, cand->num_users, H,
+                                        p.attn_tile, false, reinterpret_cast<int32_t*>(ws + p.off_work),
+                                        p.work_items, s));
+    for (int l = 0; l < c.n_layers; ++l) {
+        const LayerWeights& w = m->layers[l];
+        if (l > 0)
+            UPR_LAUNCH("rank.ln1",
+                       launch_layernorm_mx(g, ac, asc, R, d, w.ln1_g, w.ln1_b, c.ln_eps, s));
+        Epilogue e{};
+        e.mode = EPI_STORE;
+        e.acc_scale = 1.0f;
+        e.bias = w.bqkv;
+        e.out = qkv;
+        e.ldo = 3 * d;
+        e.col_scale = qscale;
+        e.scale_cols = d;
+        UPR_LAUNCH("rank.gemm_qkv", launch_gemm_mx(ac, asc, w.mx_qkv, w.mx_qkv_s, R, 3 * d, d, e, s));
+        const bf16* ck = static_cast<const bf16*>(plane_ptr(c, cache, l, 0));
+        const bf16* cv = static_cast<const bf16*>(plane_ptr(c, cache, l, 1));
+        if (p.use_mfma_attn)
+            UPR_LAUNCH("rank.attn", launch_attn_rank(qkv, o, p.row0, H, D, hist->offsets_dev,
+                                                     reinterpret_cast<const int32_t*>(ws + p.off_work),
+                                                     p.work_items, p.attn_tile, ck, cv,
+                                                     cache->capacity_rows, s));
+        else
+            UPR_LAUNCH("rank.attn",
+                       launch_attn_rank_simple<bf16, f16>(qkv, o, R, p.row0, H, D, cand->offsets_dev,
+                                                          hist->offsets_dev, cand->num_users, ck, cv,
+                                                          cache->capacity_rows, s));
+        UPR_LAUNCH("rank.quant_o", launch_mx_quantize<f16>(o, R, d, ac, asc, s));
+        Epilogue r{};
+        r.mode = EPI_RESID;
+        r.acc_scale = 1.0f;
+        r.bias = w.bo;
+        r.resid = g;
+        r.ldr = d;
+        UPR_LAUNCH("rank.gemm_o", launch_gemm_mx(ac, asc, w.mx_o, w.mx_o_s, R, d, d, r, s));
+        UPR_LAUNCH("rank.ln2", launch_layernorm_mx(g, ac, asc, R, d, w.ln2_g, w.ln2_b, c.ln_eps, s));
+        Epilogue up{};
+        up.mode = EPI_GELU_MX;
+        up.acc_scale = 1.0f;
+        up.bias = w.b1;
+        up.out = hc;
+        up.ldo = F;
+        up.out_scales = hsc;
+        UPR_LAUNCH("rank.gemm_up", launch_gemm_mx(ac, asc, w.mx_1, w.mx_1_s, R, F, d, up, s));
+        r.bias = w.b2;
+        UPR_LAUNCH("rank.gemm_down", launch_gemm_mx(hc, hsc, w.mx_2, w.mx_2_s, R, d, F, r, s));
+    }
+    return UPR_OK;
+}
 
 // Attention-output projection and FFN of one layer, on the fp32 residual g:
 // g += o Wo^T + bo;  a = LN2(g);  h = gelu(a W1^T + b1);  g += h W2^T + b2.
@@ -354,6 +487,15 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
     TA* o = reinterpret_cast<TA*>(ws + p.off_o);
     TA* h = reinterpret_cast<TA*>(ws + p.off_h);
     const float qscale = 1.4426950408889634f / std::sqrt((float)D);
+    bool mx_done = false;
+    if constexpr (std::is_same_v<Types, Bf16Types>) {
+        if (c.dtype == UPR_BF16_MXFP8) {
+            const upr_status st = rank_layers_mx(m, cache, hist, cand_emb, cand, p, ws, s);
+            if (st != UPR_OK) return st;
+            mx_done = true;
+        }
+    }
+    if (!mx_done) {
     UPR_LAUNCH("rank.init_ln1",
                launch_init_layernorm<T, TA>(cand_emb + p.row0 * d, g, a, R, d, m->layers[0].ln1_g,
                                             m->layers[0].ln1_b, c.ln_eps, s));
@@ -393,6 +535,7 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
                                                cache->capacity_rows, s));
         UPR_HIP(launch_ffn_block<Types>(kRankFfnNames, w, o, a, h, g, R, d, F, c.ln_eps, s));
     }
+    }  // !mx_done
     if (!out.heads) {
         UPR_LAUNCH("rank.score_head",
                    launch_score_head(g, out.scores + p.row0, R, d, m->fin, c.ln_eps, s));
@@ -449,7 +592,9 @@ upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
     struct LayerOff {
         size_t Wqkv, Wo, W1, W2, ln1_g, ln1_b, bqkv, bo, ln2_g, ln2_b, b1, b2;
         float s_qkv, s_o, s_1, s_2;
+        size_t mx[8];       // fp8 variant: qkv, qkv scales, o, o scales, 1, 1 scales, 2, 2 scales
     };
+    const bool mx = c.dtype == UPR_BF16_MXFP8;
     std::vector<LayerOff> lo(c.n_layers);
     const float* p = weights_host;
     std::vector<float> tmp;
@@ -477,6 +622,12 @@ upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
         lo[l].Wo = add_mat(Wo, d * d, &lo[l].s_o);
         lo[l].W1 = add_mat(W1, F * d, &lo[l].s_1);
         lo[l].W2 = add_mat(W2, d * F, &lo[l].s_2);
+        if (mx) {
+            ib.add_mx(tmp.data(), 3 * d, (int)d, &lo[l].mx[0], &lo[l].mx[1]);
+            ib.add_mx(Wo, d, (int)d, &lo[l].mx[2], &lo[l].mx[3]);
+            ib.add_mx(W1, F, (int)d, &lo[l].mx[4], &lo[l].mx[5]);
+            ib.add_mx(W2, d, (int)F, &lo[l].mx[6], &lo[l].mx[7]);
+        }
         lo[l].ln1_g = add_vec(ln1_g, d);
         lo[l].ln1_b = add_vec(ln1_b, d);
         tmp.assign(bq, bq + d);
@@ -522,6 +673,15 @@ upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
         w.ln2_b = fp(lo[l].ln2_b);
         w.b1 = fp(lo[l].b1);
         w.b2 = fp(lo[l].b2);
+        auto u8 = [&](size_t off) { return reinterpret_cast<const uint8_t*>(base + off); };
+        w.mx_qkv = mx ? u8(lo[l].mx[0]) : nullptr;
+        w.mx_qkv_s = mx ? u8(lo[l].mx[1]) : nullptr;
+        w.mx_o = mx ? u8(lo[l].mx[2]) : nullptr;
+        w.mx_o_s = mx ? u8(lo[l].mx[3]) : nullptr;
+        w.mx_1 = mx ? u8(lo[l].mx[4]) : nullptr;
+        w.mx_1_s = mx ? u8(lo[l].mx[5]) : nullptr;
+        w.mx_2 = mx ? u8(lo[l].mx[6]) : nullptr;
+        w.mx_2_s = mx ? u8(lo[l].mx[7]) : nullptr;
     }
     m->fin.lnf_g = fp(off_lnf_g);
     m->fin.lnf_b = fp(off_lnf_b);
@@ -587,7 +747,7 @@ upr_status upr_encode_user(const upr_model* m, const void* hist_emb, const upr_s
     if (p.rows == 0) return ok();
     hipStream_t s = static_cast<hipStream_t>(stream);
     char* w = static_cast<char*>(ws);
-    st = m->cfg.dtype == UPR_BF16
+    st = bf16_family(m->cfg.dtype)
              ? upr::run_encode<upr::Bf16Types>(m, static_cast<const bf16*>(hist_emb), hist, cache,
                                                p, w, s)
              : upr::run_encode<upr::F32Types>(m, static_cast<const float*>(hist_emb), hist,
@@ -625,7 +785,7 @@ upr_status upr_rank_candidates(const upr_model* m, const upr_kv_cache* cache,
     char* w = static_cast<char*>(ws);
     upr::RankOut out;
     out.scores = scores;
-    st = m->cfg.dtype == UPR_BF16
+    st = bf16_family(m->cfg.dtype)
              ? upr::run_rank<upr::Bf16Types>(m, cache, hist, static_cast<const bf16*>(cand_emb),
                                              cand, out, p, w, s)
              : upr::run_rank<upr::F32Types>(m, cache, hist, static_cast<const float*>(cand_emb),
@@ -753,7 +913,7 @@ upr_status upr_rank_actions(const upr_model* m, const upr_heads* hd, const upr_k
     out.util = utility;
     hipStream_t s = static_cast<hipStream_t>(stream);
     char* w = static_cast<char*>(ws);
-    st = m->cfg.dtype == UPR_BF16
+    st = bf16_family(m->cfg.dtype)
              ? upr::run_rank<upr::Bf16Types>(m, cache, hist, static_cast<const bf16*>(cand_emb),
                                              cand, out, p, w, s)
              : upr::run_rank<upr::F32Types>(m, cache, hist, static_cast<const float*>(cand_emb),
@@ -784,6 +944,66 @@ upr_status upr_topk_by_utility(const float* utility, const upr_segments* cand, i
                                               topk_rows, topk_utility, s);
         if (e != hipSuccess) return fail(UPR_ERR_HIP, "top-K launch failed: %s", hipGetErrorString(e));
     }
+    return ok();
+}
+
+// ---- MXFP8 encoding and the scaled fp8 linear map
+
+upr_status upr_mx_quantize_host(const float* x, int64_t rows, int32_t k, uint8_t* codes,
+                                uint8_t* scales) {
+    if (rows < 0 || k <= 0 || k % 32 != 0)
+        return fail(UPR_ERR_LIMIT, "rows %lld / k %d: need rows >= 0 and k a positive multiple of 32",
+                    (long long)rows, k);
+    if (rows > 0 && (!x || !codes || !scales)) return fail(UPR_ERR_NULL, "x, codes or scales is NULL");
+    upr::mx_quantize_host(x, rows, k, codes, scales);
+    return ok();
+}
+
+upr_status upr_mx_quantize(const void* x, int32_t in_type, int64_t rows, int32_t k, uint8_t* codes,
+                           uint8_t* scales, void* stream) {
+    if (in_type != UPR_MX_IN_F32 && in_type != UPR_MX_IN_F16 && in_type != UPR_MX_IN_BF16)
+        return fail(UPR_ERR_DTYPE, "input type %d is not a upr_mx_input value", in_type);
+    if (rows < 0 || k <= 0 || k % 32 != 0)
+        return fail(UPR_ERR_LIMIT, "rows %lld / k %d: need rows >= 0 and k a positive multiple of 32",
+                    (long long)rows, k);
+    if (rows == 0) return ok();
+    if (!x || !codes || !scales) return fail(UPR_ERR_NULL, "x, codes or scales is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    {
+        upr::ProfScope ps("mx.quantize", s);
+        e = in_type == UPR_MX_IN_F32
+                ? upr::launch_mx_quantize(static_cast<const float*>(x), rows, k, codes, scales, s)
+            : in_type == UPR_MX_IN_F16
+                ? upr::launch_mx_quantize(static_cast<const upr::f16*>(x), rows, k, codes, scales, s)
+                : upr::launch_mx_quantize(static_cast<const bf16*>(x), rows, k, codes, scales, s);
+    }
+    if (e != hipSuccess) return fail(UPR_ERR_HIP, "MXFP8 encode launch failed: %s", hipGetErrorString(e));
+    return ok();
+}
+
+upr_status upr_mx_linear(const uint8_t* a_codes, const uint8_t* a_scales, const uint8_t* w_codes,
+                         const uint8_t* w_scales, const float* bias, int64_t M, int32_t N,
+                         int32_t K, float* out, void* stream) {
+    if (M < 0 || N <= 0 || N % 8 != 0 || K <= 0 || K % 128 != 0)
+        return fail(UPR_ERR_LIMIT, "M %lld, N %d, K %d: need M >= 0, N a positive multiple of 8, "
+                    "K a positive multiple of 128", (long long)M, N, K);
+    if (M == 0) return ok();
+    if (!a_codes || !a_scales || !w_codes || !w_scales || !bias || !out)
+        return fail(UPR_ERR_NULL, "an operand pointer is NULL");
+    upr::Epilogue r{};
+    r.mode = upr::EPI_RESID;
+    r.acc_scale = 1.0f;
+    r.bias = bias;
+    r.resid = out;
+    r.ldr = N;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    {
+        upr::ProfScope ps("mx.linear", s);
+        e = upr::launch_gemm_mx(a_codes, a_scales, w_codes, w_scales, M, N, K, r, s);
+    }
+    if (e != hipSuccess) return fail(UPR_ERR_HIP, "MXFP8 GEMM launch failed: %s", hipGetErrorString(e));
     return ok();
 }
 

@@ -40,6 +40,9 @@ struct LayerWeights {
     const void* W1;
     const void* W2;
     float s_qkv, s_o, s_1, s_2;
+    // fp8 projection variant: the same matrices as MXFP8 (E4M3 codes
+    // [out, in], E8M0 scales [out, in / 32]); null for other models
+    const uint8_t *mx_qkv, *mx_qkv_s, *mx_o, *mx_o_s, *mx_1, *mx_1_s, *mx_2, *mx_2_s;
     const float* ln1_g;
     const float* ln1_b;
     const float* bqkv;      // [3d]: bq, bk, bv
@@ -76,6 +79,8 @@ enum EpiMode : int {
     EPI_RESID = 2,      // resid[m, n] += .           (fp32, in place)
     EPI_QKV_CACHE = 3,  // columns [0,d): query -> out (scaled); [d,2d): keys and
                         // [2d,3d): values -> cache plane of the layer
+    EPI_GELU_MX = 4,    // gelu_tanh(.) as MXFP8: E4M3 codes -> out (ldo bytes per
+                        // row), one E8M0 byte per 32 columns -> out_scales
 };
 
 struct Epilogue {
@@ -95,6 +100,8 @@ struct Epilogue {
     int64_t row0;
     int d_model;
     int head_dim;
+    // EPI_GELU_MX: block scales, ldo / 32 bytes per row
+    void* out_scales;
 };
 
 // ---------------------------------------------------------------------------
@@ -110,6 +117,26 @@ hipError_t launch_layernorm(const float* g, TA* a, int64_t rows, int d, const fl
                             const float* shift, float eps, hipStream_t s);
 hipError_t launch_score_head(const float* g, float* scores, int64_t rows, int d,
                              const FinalWeights& fw, float eps, hipStream_t s);
+
+// MXFP8 variants of the LayerNorm launches (d a multiple of 256): codes
+// [rows, d], scales [rows, d / 32].
+template <typename TKV>
+hipError_t launch_init_layernorm_mx(const TKV* x, float* g, uint8_t* codes, uint8_t* scales,
+                                    int64_t rows, int d, const float* gain, const float* shift,
+                                    float eps, hipStream_t s);
+hipError_t launch_layernorm_mx(const float* g, uint8_t* codes, uint8_t* scales, int64_t rows,
+                               int d, const float* gain, const float* shift, float eps,
+                               hipStream_t s);
+// MXFP8 encoding of x [rows, k] (k a multiple of 32) along its rows.
+template <typename T>
+hipError_t launch_mx_quantize(const T* x, int64_t rows, int k, uint8_t* codes, uint8_t* scales,
+                              hipStream_t s);
+// MXFP8 projection GEMM: out = A W^T + epilogue with A [M, K] and W [N, K]
+// E4M3 codes and their E8M0 scales ([M, K/32], [N, K/32]); K a multiple of
+// 128; epilogue modes EPI_STORE, EPI_RESID and EPI_GELU_MX.
+hipError_t launch_gemm_mx(const uint8_t* A, const uint8_t* A_scales, const uint8_t* W,
+                          const uint8_t* W_scales, int64_t M, int N, int K, const Epilogue& epi,
+                          hipStream_t s);
 
 // Reference-quality GEMM: out = A[M,K] W[N,K]^T + epilogue; A and W are of the
 // projection operand type TA, kv-typed epilogue outputs of type TKV.

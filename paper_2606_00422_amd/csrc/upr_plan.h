@@ -34,7 +34,10 @@ struct RankPlan {
     size_t bytes = 0;
 };
 
-inline size_t dtype_bytes(const upr_config& c) { return c.dtype == UPR_BF16 ? 2 : 4; }
+inline bool bf16_storage(const upr_config& c) {
+    return c.dtype == UPR_BF16 || c.dtype == UPR_BF16_MXFP8;
+}
+inline size_t dtype_bytes(const upr_config& c) { return bf16_storage(c) ? 2 : 4; }
 
 // Number of MFMA attention work items over the rows of `offs`: one per
 // (user, head, tile of up to kAttnTile rows).
@@ -45,7 +48,7 @@ inline int64_t attn_items(const upr_config& c, int U, const int32_t* offs) {
 }
 
 inline bool use_mfma_attn(const upr_config& c) {
-    return kHaveMfmaAttn && c.dtype == UPR_BF16 && c.head_dim == 64;
+    return kHaveMfmaAttn && bf16_storage(c) && c.head_dim == 64;
 }
 
 // Workspace of encode for the history rows of `hoffs` (host offsets): fp32
@@ -73,7 +76,10 @@ inline EncodePlan plan_encode(const upr_config& c, int U, const int32_t* hoffs) 
 // Workspace of rank for the candidate rows of `coffs` (host offsets):
 // residual, LayerNorm output, fused q|k|v rows, attention output, FFN hidden
 // (at least head_cols wide: the action heads' hidden layer reuses it), and
-// (bf16 models) the attention work list.
+// (bf16 models) the attention work list.  The fp8-projection variant keeps
+// MXFP8 encodings in the LayerNorm-output and FFN-hidden buffers (codes,
+// then scales at the next 256-byte boundary: rows x cols x 2 bytes hold
+// both for rows x cols >= 256).
 inline RankPlan plan_rank(const upr_config& c, int U, const int32_t* coffs, int head_cols = 0) {
     RankPlan p;
     p.row0 = coffs[0];
@@ -99,7 +105,8 @@ template <typename TA, typename TKV>
 hipError_t launch_gemm(const TA* A, int64_t lda, const TA* W, int64_t M, int N, int K,
                        const Epilogue& epi, hipStream_t s);
 
-// fp16 MFMA GEMM (K a multiple of 64, lda a multiple of 8).
+// fp16 MFMA GEMM (K a multiple of 64, lda a multiple of 8).  (The MXFP8
+// GEMM, launch_gemm_mx, is declared with the other launchers.)
 hipError_t launch_gemm_mfma(const f16* A, int64_t lda, const f16* W, int64_t M, int N, int K,
                             const Epilogue& epi, hipStream_t s);
 
@@ -123,6 +130,10 @@ hipError_t launch_attn_encode(const bf16* q, f16* o, int64_t row0, int H, int D,
                               const int32_t* hist_offsets, const int32_t* work, int64_t items,
                               int tile, const bf16* cache_k, const bf16* cache_v,
                               int64_t cache_cap, hipStream_t s);
+
+// Host MXFP8 encoding of x [rows, k] (k a multiple of 32): the weights of
+// the fp8-projection variant, and upr_mx_quantize_host.
+void mx_quantize_host(const float* x, int64_t rows, int k, uint8_t* codes, uint8_t* scales);
 
 // Per-action heads: at most kMaxActions heads; utility weights by value.
 constexpr int kMaxActions = 8;

@@ -19,7 +19,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libupr.so")
 UPR_OK, UPR_ERR_NULL, UPR_ERR_CONFIG, UPR_ERR_OFFSETS, UPR_ERR_CAPACITY = 0, 1, 2, 3, 4
 UPR_ERR_WORKSPACE, UPR_ERR_DTYPE, UPR_ERR_HIP, UPR_ERR_WEIGHTS, UPR_ERR_LIMIT = 5, 6, 7, 8, 9
 UPR_TOPK_MAX_CANDIDATES = 16384
-UPR_F32, UPR_BF16 = 0, 1
+UPR_F32, UPR_BF16, UPR_BF16_MXFP8 = 0, 1, 2
+UPR_MX_IN_F32, UPR_MX_IN_F16, UPR_MX_IN_BF16 = 0, 1, 2
 
 # Every symbol include/upr.h declares.
 EXPORTS = (
@@ -29,6 +30,7 @@ EXPORTS = (
     "upr_profile_enable", "upr_profile_read",
     "upr_heads_weights_count", "upr_heads_create", "upr_heads_destroy",
     "upr_rank_actions_workspace_bytes", "upr_rank_actions", "upr_topk_by_utility",
+    "upr_mx_quantize_host", "upr_mx_quantize", "upr_mx_linear",
 )
 
 
@@ -96,6 +98,9 @@ def load(path: str = LIB_PATH):
         "upr_rank_actions_workspace_bytes": (SZ, [VP, VP, segp, segp]),
         "upr_rank_actions": (I32, [VP, VP, cachep, segp, VP, segp, VP, VP, VP, VP, SZ, VP]),
         "upr_topk_by_utility": (I32, [VP, segp, I32, VP, VP, VP]),
+        "upr_mx_quantize_host": (I32, [VP, I64, I32, VP, VP]),
+        "upr_mx_quantize": (I32, [VP, I32, I64, I32, VP, VP, VP]),
+        "upr_mx_linear": (I32, [VP, VP, VP, VP, VP, I64, I32, I32, VP, VP]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -116,11 +121,15 @@ def _check(status: int):
 # The C calls, same names, plain arguments
 # ---------------------------------------------------------------------------
 
+DTYPES = {"f32": UPR_F32, "bf16": UPR_BF16, "bf16_mxfp8": UPR_BF16_MXFP8}
+
+
 def make_config(d_model, n_heads, n_layers, d_ff, dtype, ln_eps=1e-5) -> upr_config:
+    """dtype: "f32", "bf16", "bf16_mxfp8" or a upr_dtype value."""
     if d_model % n_heads:
         raise ValueError("d_model must be a multiple of n_heads")
-    return upr_config(d_model, n_heads, d_model // n_heads, n_layers, d_ff,
-                      UPR_BF16 if dtype in ("bf16", UPR_BF16) else UPR_F32, ln_eps)
+    code = DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
+    return upr_config(d_model, n_heads, d_model // n_heads, n_layers, d_ff, code, ln_eps)
 
 
 def upr_weights_count(cfg: upr_config) -> int:
@@ -249,6 +258,54 @@ def _check_tensor(t, name, dtype=None):
         raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
 
 
+def upr_mx_quantize_host(x: np.ndarray):
+    """Host MXFP8 encoding of x [rows, k] (float32): (codes uint8 [rows, k],
+    scales uint8 [rows, k / 32])."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    rows, k = x.shape
+    codes = np.empty((rows, k), dtype=np.uint8)
+    scales = np.empty((rows, max(k // 32, 0)), dtype=np.uint8)
+    _check(load().upr_mx_quantize_host(x.ctypes.data, rows, k, codes.ctypes.data, scales.ctypes.data))
+    return codes, scales
+
+
+def upr_mx_quantize(x, codes, scales, stream=None):
+    """Device MXFP8 encoding of the 2-D tensor x (float32 / float16 /
+    bfloat16) into uint8 tensors codes [rows, k] and scales [rows, k / 32]."""
+    import torch
+    kinds = {torch.float32: UPR_MX_IN_F32, torch.float16: UPR_MX_IN_F16,
+             torch.bfloat16: UPR_MX_IN_BF16}
+    for t, name in ((x, "x"), (codes, "codes"), (scales, "scales")):
+        if not (t.is_cuda and t.is_contiguous()):
+            raise ValueError(f"{name} must be a contiguous GPU tensor")
+    if x.dtype not in kinds or codes.dtype != torch.uint8 or scales.dtype != torch.uint8:
+        raise ValueError("x must be float32/float16/bfloat16, codes and scales uint8")
+    rows, k = x.shape
+    if tuple(codes.shape) != (rows, k) or tuple(scales.shape) != (rows, k // 32):
+        raise ValueError("codes must be [rows, k] and scales [rows, k / 32]")
+    _check(load().upr_mx_quantize(x.data_ptr(), kinds[x.dtype], rows, k, codes.data_ptr(),
+                                  scales.data_ptr(), current_stream() if stream is None else stream))
+
+
+def upr_mx_linear(a_codes, a_scales, w_codes, w_scales, bias, out, stream=None):
+    """out [M, N] += A W^T + bias with MXFP8 operands (uint8 GPU tensors
+    a_codes [M, K], a_scales [M, K/32], w_codes [N, K], w_scales [N, K/32];
+    bias [N] and out float32)."""
+    import torch
+    M, K = a_codes.shape
+    N = w_codes.shape[0]
+    for t, shape, dt, name in ((a_codes, (M, K), torch.uint8, "a_codes"),
+                               (a_scales, (M, K // 32), torch.uint8, "a_scales"),
+                               (w_codes, (N, K), torch.uint8, "w_codes"),
+                               (w_scales, (N, K // 32), torch.uint8, "w_scales"),
+                               (bias, (N,), torch.float32, "bias"), (out, (M, N), torch.float32, "out")):
+        if not (t.is_cuda and t.is_contiguous()) or t.dtype != dt or tuple(t.shape) != shape:
+            raise ValueError(f"{name} must be a contiguous GPU {dt} tensor of shape {shape}")
+    _check(load().upr_mx_linear(a_codes.data_ptr(), a_scales.data_ptr(), w_codes.data_ptr(),
+                                w_scales.data_ptr(), bias.data_ptr(), M, N, K, out.data_ptr(),
+                                current_stream() if stream is None else stream))
+
+
 def current_stream() -> int:
     import torch
     return int(torch.cuda.current_stream().cuda_stream)
@@ -260,7 +317,7 @@ class Model:
     def __init__(self, cfg: upr_config, weights: np.ndarray):
         self.cfg = cfg
         self.handle = upr_model_create(cfg, weights)
-        self.torch_dtype = "bfloat16" if cfg.dtype == UPR_BF16 else "float32"
+        self.torch_dtype = "bfloat16" if cfg.dtype in (UPR_BF16, UPR_BF16_MXFP8) else "float32"
 
     def close(self):
         if self.handle:
@@ -275,7 +332,7 @@ class Model:
 
     def new_cache(self, capacity_rows: int):
         import torch
-        dt = torch.bfloat16 if self.cfg.dtype == UPR_BF16 else torch.float32
+        dt = torch.bfloat16 if self.cfg.dtype in (UPR_BF16, UPR_BF16_MXFP8) else torch.float32
         c = self.cfg
         cache = torch.zeros((c.n_layers, 2, c.n_heads, capacity_rows, c.head_dim), dtype=dt,
                             device="cuda")

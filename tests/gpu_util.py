@@ -20,10 +20,11 @@ def say(msg):
 class GpuRun:
     """Device buffers of one problem plus a model; encode/rank through the C ABI."""
 
-    def __init__(self, inp, capacity_rows=None):
+    def __init__(self, inp, capacity_rows=None, model_dtype=None):
         import torch
         self.inp = inp
-        self.cfg = upr.make_config(inp.d, inp.H, inp.L, inp.F, inp.dtype)
+        self.cfg = upr.make_config(inp.d, inp.H, inp.L, inp.F,
+                                   inp.dtype if model_dtype is None else model_dtype)
         self.model = upr.Model(self.cfg, inp.weights)
         self.tdt = torch.bfloat16 if inp.dtype == "bf16" else torch.float32
         dev = "cuda"

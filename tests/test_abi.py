@@ -59,6 +59,8 @@ def test_cache_bytes_and_index():
     (dict(d_ff=100), upr.UPR_ERR_CONFIG),
     (dict(dtype=7), upr.UPR_ERR_DTYPE),
     (dict(ln_eps=0.0), upr.UPR_ERR_CONFIG),
+    (dict(dtype=upr.UPR_BF16_MXFP8), upr.UPR_ERR_CONFIG),                   # d 128: not % 256
+    (dict(dtype=upr.UPR_BF16_MXFP8, d_model=256, n_heads=4, d_ff=320), upr.UPR_ERR_CONFIG),  # F % 128
 ])
 def test_model_create_rejects_bad_configs(kw, status):
     base = dict(d_model=128, n_heads=2, head_dim=64, n_layers=1, d_ff=256, dtype=upr.UPR_BF16,
@@ -92,3 +94,38 @@ def test_null_model_is_rejected_before_any_launch():
     assert st == upr.UPR_ERR_NULL
     assert upr.upr_rank_workspace_bytes(0, seg, seg) == 0
     assert upr.upr_status_string(upr.UPR_ERR_OFFSETS) == "malformed segment offsets"
+
+
+def test_host_mx_encoding_matches_the_oracle_bit_for_bit():
+    """upr_mx_quantize_host (host logic: the fp8 variant's weight encoding)
+    against oracle.mx_quantize on float32 values, including saturating block
+    tops, subnormal-range values, zeros and negative zeros."""
+    import oracle
+    rng = np.random.default_rng(31)
+    x = (rng.standard_normal((64, 256)) * np.exp2(rng.integers(-30, 30, (64, 1)))).astype(np.float32)
+    x[0] = 0.0
+    x[1, :32] = -0.0
+    x[2, 5] = 1e-42                      # subnormal float32 block maximum
+    x[3, :32] = rng.uniform(-1, 1, 32).astype(np.float32) * np.float32(2.0 ** -140)
+    x[4, 7] = 3.0e38
+    codes, scales = upr.upr_mx_quantize_host(x)
+    oc, os_ = oracle.mx_quantize(x.astype(np.float64))
+    np.testing.assert_array_equal(codes, oc)
+    np.testing.assert_array_equal(scales, os_)
+
+
+def test_mx_calls_validate_before_any_launch():
+    for k in (0, 33, -32):
+        with pytest.raises(upr.UprError) as ei:
+            upr.upr_mx_quantize_host(np.zeros((2, max(k, 1)), np.float32)[:, :0] if k <= 0 else
+                                     np.zeros((2, k), np.float32))
+        assert ei.value.status == upr.UPR_ERR_LIMIT
+    lib = upr.load()
+    assert lib.upr_mx_quantize(None, 9, 1, 32, None, None, None) == upr.UPR_ERR_DTYPE
+    assert lib.upr_mx_quantize(None, upr.UPR_MX_IN_F32, 4, 48, None, None, None) == upr.UPR_ERR_LIMIT
+    assert lib.upr_mx_quantize(None, upr.UPR_MX_IN_F32, 4, 64, None, None, None) == upr.UPR_ERR_NULL
+    assert lib.upr_mx_quantize(None, upr.UPR_MX_IN_F32, 0, 64, None, None, None) == upr.UPR_OK
+    assert lib.upr_mx_linear(None, None, None, None, None, 4, 16, 96, None, None) == upr.UPR_ERR_LIMIT
+    assert lib.upr_mx_linear(None, None, None, None, None, 4, 12, 128, None, None) == upr.UPR_ERR_LIMIT
+    assert lib.upr_mx_linear(None, None, None, None, None, 4, 16, 128, None, None) == upr.UPR_ERR_NULL
+    assert lib.upr_mx_linear(None, None, None, None, None, 0, 16, 128, None, None) == upr.UPR_OK

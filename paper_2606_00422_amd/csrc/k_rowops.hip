@@ -20,6 +20,15 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 template <typename T> __device__ __forceinline__ float to_f(T v) { return (float)v; }
 
+// Four consecutive token values (8 bytes for bf16, 16 for fp32) as floats.
+template <typename T>
+__device__ __forceinline__ void load4(const T* __restrict__ p, float* v) {
+    typedef __attribute__((ext_vector_type(4))) T t4;
+    const t4 x = *reinterpret_cast<const t4*>(p);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) v[t] = (float)x[t];
+}
+
 constexpr int kRowsPerBlock = 4;     // 4 waves, one row each
 constexpr int kMaxPerLane = 16;      // d <= 1024
 
@@ -142,12 +151,15 @@ __global__ __launch_bounds__(256) void k_init_layernorm(const TKV* __restrict__ 
     float v[kMaxPerLane];
     const TKV* xr = x + row * d;
     float* gr = g + row * d;
+    if (VEC) {
 #pragma unroll
-    for (int i = 0; i < kMaxPerLane; ++i)
-        if (i < per) {
-            const int c = feat<VEC>(lane, i);
-            v[i] = to_f(xr[c]);
-        }
+        for (int j = 0; j < kMaxPerLane / 4; ++j)
+            if (4 * j < per) load4(xr + j * 256 + 4 * lane, v + 4 * j);
+    } else {
+#pragma unroll
+        for (int i = 0; i < kMaxPerLane; ++i)
+            if (i < per) v[i] = to_f(xr[lane + 64 * i]);
+    }
     if (VEC) {
 #pragma unroll
         for (int j = 0; j < kMaxPerLane / 4; ++j)
@@ -199,8 +211,7 @@ __global__ __launch_bounds__(256) void k_layernorm_mx(const TKV* __restrict__ x,
         for (int j = 0; j < kMaxPerLane / 4; ++j)
             if (4 * j < per) {
                 const int c = j * 256 + 4 * lane;
-#pragma unroll
-                for (int t = 0; t < 4; ++t) v[4 * j + t] = to_f(xr[c + t]);
+                load4(xr + c, v + 4 * j);
                 *reinterpret_cast<float4*>(gr + c) =
                     make_float4(v[4 * j], v[4 * j + 1], v[4 * j + 2], v[4 * j + 3]);
             }

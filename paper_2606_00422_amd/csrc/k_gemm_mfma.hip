@@ -97,18 +97,18 @@ __device__ __forceinline__ float gelu_fast(float x) {
     return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * t));
 }
 
-// Two values rounded to bf16 (BF) or fp16, packed low-first.
+// Two values rounded to bf16 (BF) or fp16, packed low-first (one
+// v_cvt_pk_{bf16,f16}_f32, round to nearest even).
 template <bool BF>
 __device__ __forceinline__ unsigned pack2(float a, float b) {
-    unsigned short x, y;
-    if constexpr (BF) {
-        x = __builtin_bit_cast(unsigned short, (__bf16)keep_f32(a));
-        y = __builtin_bit_cast(unsigned short, (__bf16)keep_f32(b));
-    } else {
-        x = __builtin_bit_cast(unsigned short, (_Float16)keep_f32(a));
-        y = __builtin_bit_cast(unsigned short, (_Float16)keep_f32(b));
-    }
-    return (unsigned)x | ((unsigned)y << 16);
+    typedef __attribute__((ext_vector_type(2))) float f2;
+    typedef __attribute__((ext_vector_type(2))) __bf16 bf2;
+    typedef __attribute__((ext_vector_type(2))) _Float16 hf2;
+    const f2 v = {keep_f32(a), keep_f32(b)};
+    if constexpr (BF)
+        return __builtin_bit_cast(unsigned, __builtin_convertvector(v, bf2));
+    else
+        return __builtin_bit_cast(unsigned, __builtin_convertvector(v, hf2));
 }
 
 // Epilogue of one wave's 128 x 64 tile (acc in the transposed MFMA layout:
@@ -140,16 +140,24 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
         const float4 bias4 = col_ok ? *reinterpret_cast<const float4*>(epi.bias + col)
                                     : make_float4(0.f, 0.f, 0.f, 0.f);
         float* const st = reinterpret_cast<float*>(region);
-        float4 g[8], gn[8];
+        // The wave tile's residual rows through a buffer descriptor whose
+        // range ends at row M: rows past the end load zeros and their stores
+        // are dropped, so the passes need no branches and the wait before a
+        // pass's stores can leave the next pass's loads in flight.  Lanes
+        // whose columns lie past N address beyond the range.
+        const int64_t rows_valid = M - wrow0 < 0 ? 0 : (M - wrow0 < kWM ? M - wrow0 : kWM);
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            epi.resid + wrow0 * epi.ldr, (short)0, (int)(rows_valid * epi.ldr * 4), 0x00020000);
+        const unsigned ldr4 = (unsigned)epi.ldr * 4u;
+        const unsigned vo = col_ok ? (unsigned)rsub * ldr4 + (unsigned)col * 4u : 0x80000000u;
+        float4 g[2][8];                     // residual rows of passes i (even/odd)
         auto load_resid = [&](int i, float4 (&dst)[8]) {
 #pragma unroll
-            for (int p = 0; p < 8; ++p) {
-                const int64_t row = wrow0 + i * 32 + p * 4 + rsub;
-                if (row < M && col_ok)
-                    dst[p] = *reinterpret_cast<const float4*>(epi.resid + row * epi.ldr + col);
-            }
+            for (int p = 0; p < 8; ++p)
+                dst[p] = __builtin_bit_cast(
+                    float4, __builtin_amdgcn_raw_buffer_load_b128(rs, vo + (unsigned)(i * 32 + p * 4) * ldr4, 0, 0));
         };
-        load_resid(0, g);
+        load_resid(0, g[0]);
 #pragma unroll
         for (int i = 0; i < kTM; ++i) {
 #pragma unroll
@@ -162,21 +170,20 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
                 }
             __builtin_amdgcn_s_waitcnt(0xC07F);
             __builtin_amdgcn_wave_barrier();
-            if (i + 1 < kTM) load_resid(i + 1, gn);
+            if (i + 1 < kTM) load_resid(i + 1, g[(i + 1) & 1]);
             float4 x[8];
 #pragma unroll
             for (int p = 0; p < 8; ++p)
                 x[p] = *reinterpret_cast<const float4*>(st + (p * 4 + rsub) * kStage32 + ch * 4);
 #pragma unroll
             for (int p = 0; p < 8; ++p) {
-                const int64_t row = wrow0 + i * 32 + p * 4 + rsub;
-                if (row >= M || !col_ok) continue;
-                const f32x4 o = {g[p].x + fmaf(x[p].x, sc, bias4.x), g[p].y + fmaf(x[p].y, sc, bias4.y),
-                                 g[p].z + fmaf(x[p].z, sc, bias4.z), g[p].w + fmaf(x[p].w, sc, bias4.w)};
-                __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(epi.resid + row * epi.ldr + col));
+                const float4 r = g[i & 1][p];
+                const u32x4 o = __builtin_bit_cast(
+                    u32x4, make_float4(r.x + fmaf(x[p].x, sc, bias4.x), r.y + fmaf(x[p].y, sc, bias4.y),
+                                       r.z + fmaf(x[p].z, sc, bias4.z), r.w + fmaf(x[p].w, sc, bias4.w)));
+                __builtin_amdgcn_raw_buffer_store_b128(o, rs, vo + (unsigned)(i * 32 + p * 4) * ldr4, 0,
+                                                       2 /* nt */);
             }
-#pragma unroll
-            for (int p = 0; p < 8; ++p) g[p] = gn[p];
             __builtin_amdgcn_s_waitcnt(0xC07F);
             __builtin_amdgcn_wave_barrier();
         }
@@ -238,19 +245,50 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
                     (unsigned short)sc2;
         }
     } else {
+        // Per run of four columns: multiplier and bias.  EPI_STORE scales
+        // columns < scale_cols by col_scale, EPI_QKV_CACHE the query columns
+        // (< d_model); both fold the factor into multiplier and bias.
         float4 bq[kTN][4];
+        float cq[kTN][4];
 #pragma unroll
         for (int j = 0; j < kTN; ++j)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int col = wcol0 + j * 32 + 8 * q + 4 * lhalf;
-                bq[j][q] = col < N ? *reinterpret_cast<const float4*>(epi.bias + col)
+                float4 b = col < N ? *reinterpret_cast<const float4*>(epi.bias + col)
                                    : make_float4(0.f, 0.f, 0.f, 0.f);
+                float c = sc;
+                if constexpr (MODE != EPI_GELU) {
+                    const int lim = MODE == EPI_STORE ? epi.scale_cols : epi.d_model;
+                    const float cs = col < lim ? epi.col_scale : 1.0f;
+                    c = sc * cs;
+                    b = make_float4(b.x * cs, b.y * cs, b.z * cs, b.w * cs);
+                }
+                bq[j][q] = b;
+                cq[j][q] = c;
             }
         constexpr bool kBf = MODE != EPI_GELU;
         unsigned short* const st = reinterpret_cast<unsigned short*>(region);
         const int ch = lane & 7, rs = lane >> 3;
         const int col = wcol0 + ch * 8;
+        // Staged rows come back as row lr0 + off of the wave tile, lane
+        // (ch, rs) holding columns col .. col+7; the destination of row
+        // wrow0 + lr0 + off is obase + off * ostride.
+        const int lr0 = (rs >> 1) + 8 * (rs & 1);
+        const int rows_left = (int)min(M - wrow0 - lr0, (int64_t)kBM);
+        unsigned short* obase = static_cast<unsigned short*>(epi.out) + (wrow0 + lr0) * epi.ldo + col;
+        int64_t ostride = epi.ldo;
+        if constexpr (MODE == EPI_QKV_CACHE) {
+            const int d = epi.d_model;
+            if (col >= d) {   // 8 columns never straddle a head (head_dim % 8 == 0)
+                const int part = col >= 2 * d ? 2 : 1;
+                const int c = col - part * d;
+                const int h = c / epi.head_dim, e = c - h * epi.head_dim;
+                unsigned short* plane = static_cast<unsigned short*>(part == 1 ? epi.cache_k : epi.cache_v);
+                obase = plane + ((int64_t)h * epi.cache_cap + (epi.row0 + wrow0 + lr0)) * epi.head_dim + e;
+                ostride = epi.head_dim;
+            }
+        }
 #pragma unroll
         for (int i = 0; i < kTM; ++i) {
 #pragma unroll
@@ -259,21 +297,13 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     float v[4];
-                    v[0] = fmaf(acc[j][i][4 * q + 0], sc, bq[j][q].x);
-                    v[1] = fmaf(acc[j][i][4 * q + 1], sc, bq[j][q].y);
-                    v[2] = fmaf(acc[j][i][4 * q + 2], sc, bq[j][q].z);
-                    v[3] = fmaf(acc[j][i][4 * q + 3], sc, bq[j][q].w);
+                    v[0] = fmaf(acc[j][i][4 * q + 0], cq[j][q], bq[j][q].x);
+                    v[1] = fmaf(acc[j][i][4 * q + 1], cq[j][q], bq[j][q].y);
+                    v[2] = fmaf(acc[j][i][4 * q + 2], cq[j][q], bq[j][q].z);
+                    v[3] = fmaf(acc[j][i][4 * q + 3], cq[j][q], bq[j][q].w);
                     if constexpr (MODE == EPI_GELU) {
 #pragma unroll
                         for (int r = 0; r < 4; ++r) v[r] = gelu_fast(v[r]);
-                    } else {
-                        // EPI_STORE: columns < scale_cols scaled; EPI_QKV_CACHE:
-                        // the query columns (< d_model) scaled
-                        const int c4 = wcol0 + j * 32 + 8 * q + 4 * lhalf;
-                        const int lim = MODE == EPI_STORE ? epi.scale_cols : epi.d_model;
-                        const float cs = c4 < lim ? epi.col_scale : 1.0f;
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) v[r] = v[r] * cs;
                     }
                     pk[q][0] = pack2<kBf>(v[0], v[1]);
                     pk[q][1] = pack2<kBf>(v[2], v[3]);
@@ -295,27 +325,10 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
             __builtin_amdgcn_wave_barrier();
 #pragma unroll
             for (int p = 0; p < 4; ++p) {
-                const int rl = 16 * (p >> 1) + 4 * (p & 1) + (rs >> 1) + 8 * (rs & 1);
-                const u32x4 o = *reinterpret_cast<const u32x4*>(st + rl * kStage16 + ch * 8);
-                const int64_t row = wrow0 + i * 32 + rl;
-                if (row >= M || col >= N) continue;          // N is a multiple of 8
-                unsigned short* dst;
-                if constexpr (MODE == EPI_QKV_CACHE) {
-                    const int d = epi.d_model;
-                    if (col < d) {
-                        dst = static_cast<unsigned short*>(epi.out) + row * epi.ldo + col;
-                    } else {   // 8 columns never straddle a head (head_dim % 8 == 0)
-                        const int part = col >= 2 * d ? 2 : 1;
-                        const int c = col - part * d;
-                        const int h = c / epi.head_dim, e = c - h * epi.head_dim;
-                        unsigned short* plane =
-                            static_cast<unsigned short*>(part == 1 ? epi.cache_k : epi.cache_v);
-                        dst = plane + ((int64_t)h * epi.cache_cap + (epi.row0 + row)) * epi.head_dim + e;
-                    }
-                } else {
-                    dst = static_cast<unsigned short*>(epi.out) + row * epi.ldo + col;
-                }
-                __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(dst));
+                const int off = i * 32 + 16 * (p >> 1) + 4 * (p & 1);
+                const u32x4 o = *reinterpret_cast<const u32x4*>(st + (off - i * 32 + lr0) * kStage16 + ch * 8);
+                if (off >= rows_left || col >= N) continue;          // N is a multiple of 8
+                __builtin_nontemporal_store(o, reinterpret_cast<u32x4*>(obase + off * ostride));
             }
             __builtin_amdgcn_s_waitcnt(0xC07F);
             __builtin_amdgcn_wave_barrier();

@@ -208,6 +208,9 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
         if (!wave_active || (CAUSAL && kabs > wave_last)) return;   // nothing to do for this wave
         // S^T - m for 32 keys x 64 queries
         f32x4 s[4][2];
+        // The MFMA runs of a wave take issue priority over the other wave on
+        // its SIMD, whose exponentials then fill the matrix core's gaps.
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
             b8 kf[2];
@@ -221,6 +224,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
                 s[qg][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[1], qf[qg][1], acc, 0, 0, 0);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
         // ranking: mask keys past the history end (last sub-block only);
         // encode: mask keys after the query (diagonal sub-blocks only)
         if (__builtin_expect(CAUSAL ? kabs + 31 > ipos0 + wave * kQW : kabs + 32 > n, 0)) {
@@ -251,6 +255,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
         // O^T += V^T P^T.  V^T fragment of e-block eb: lane (g, i) needs
         // V[key(8g + j)][16eb + i]; in each 16-lane group, lane s of a
         // transposing read addresses row 4g + s/4 (+16), dims 16eb + 4(s%4).
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int eb = 0; eb < 4; ++eb) {
             b8 vf;
@@ -268,6 +273,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
             for (int qg = 0; qg < 4; ++qg)
                 o[qg][eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qg], o[qg][eb], 0, 0, 0);
         }
+        __builtin_amdgcn_s_setprio(0);
     };
 
     auto stage = [&](const bf16* cK, const bf16* cV, bf16* nK, bf16* nV, int st) __attribute__((always_inline)) {

@@ -26,6 +26,15 @@
 // stores are non-temporal, so the output stream does not evict the operand
 // panels that later tiles re-read from L2.
 //
+// Residual update with LayerNorm (EPI_RESID_LN: the LayerNorm that follows
+// the output projection and the FFN down projection).  LayerNorm needs whole
+// rows, so this mode takes a 128 x 512 tile (rows of at most 512 values) with
+// the eight waves side by side along N, each still 128 x 64.  After a 32-row
+// pass of the residual update, each wave reduces per-row mean and squared
+// deviations over its columns, the waves exchange them through LDS at a
+// workgroup barrier, and each writes the normalized values of its columns as
+// fp16: the updated residual is never read back from HBM.
+//
 // Tile order is XCD-aware: workgroup b runs on XCD b % 8 and the tiles are
 // renumbered so each XCD sweeps a contiguous range of (M-panel, N-tile)
 // pairs; the N-tiles of one A row-panel then share one L2.
@@ -57,14 +66,22 @@ typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(8))) int i32x8;
 typedef __attribute__((ext_vector_type(4))) int i32x4;
 
-constexpr int kBM = 256, kBN = 256, kBK = 64;     // block tile
+constexpr int kBK = 64;                            // K-step (fp16 values)
 constexpr int kThreads = 512;                      // 8 waves
-constexpr int kWavesN = 4;
 constexpr int kWM = 128, kWN = 64;                 // per-wave tile
 constexpr int kTM = kWM / 32, kTN = kWN / 32;      // 32x32 MFMA tiles per wave
 constexpr int kCPR = kBK / 8;                      // 16-byte chunks per LDS row (8)
-constexpr int kLoadsA = 2 * kBM * kCPR / kThreads; // per leading wave per K-step (8)
-constexpr int kLoadsB = 2 * kBN * kCPR / kThreads;
+// Block tile by epilogue: 256 x 256 in a 2 (M) x 4 (N) wave grid; the
+// residual update with LayerNorm needs whole rows in one workgroup, so it
+// takes 128 x 512 with the eight waves side by side along N.  Loads per
+// leading wave per K-step: rows / 32 (a load fills 8 rows, four leading waves).
+template <int MODE>
+struct Shape {
+    static constexpr bool kWide = MODE == EPI_RESID_LN;
+    static constexpr int kBM = kWide ? 128 : 256, kBN = kWide ? 512 : 256;
+    static constexpr int kWavesN = kWide ? 8 : 4;
+    static constexpr int kLoadsA = kBM * kCPR / (kThreads / 2), kLoadsB = kBN * kCPR / (kThreads / 2);
+};
 // Epilogue staging row strides (elements).  fp32: 272 bytes, so the 16 rows
 // written by one 16-lane group of 16-byte stores fall on distinct bank
 // groups; 16-bit: 144 bytes, likewise, and rows 8 apart land on disjoint
@@ -127,13 +144,24 @@ __device__ __forceinline__ unsigned pack2(float a, float b) {
 // v_permlane32_swap so each lane holds eight consecutive columns (16 bytes)
 // and the staged rows (32 x 144 bytes) are written back as 128-byte
 // segments, 16 bytes per lane (narrower stores measured slower).
+//
+// Residual update with LayerNorm (whole rows in the workgroup, the eight
+// waves side by side along N): after a pass's updated rows are stored, each
+// wave reduces, per row, the mean and the sum of squared deviations of its
+// (up to) 64 columns; the waves exchange them through `lnx` at a workgroup
+// barrier, and each combines the eight partials (Chan et al.'s pairwise
+// update: M2 = sum M2_w + n_w (mean_w - mean)^2) into the row's mean and
+// 1/sqrt(var + eps), then writes LN of its columns.  wn: the wave's column
+// block within the tile.
 template <int MODE>
 __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* const region,
                                            int64_t wrow0, int wcol0, int64_t M, int N,
-                                           const Epilogue& epi, int lane) {
+                                           const Epilogue& epi, int lane, float* const lnx, int wn,
+                                           bool lead) {
     const int lrow = lane & 31, lhalf = lane >> 5;
     const float sc = epi.acc_scale;
-    if constexpr (MODE == EPI_RESID) {
+    (void)lead;
+    if constexpr (MODE == EPI_RESID || MODE == EPI_RESID_LN) {
         const int ch = lane & 15, rsub = lane >> 4;
         const int col = wcol0 + ch * 4;
         const bool col_ok = col < N;                  // N is a multiple of 8
@@ -156,6 +184,88 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
             for (int p = 0; p < 8; ++p)
                 dst[p] = __builtin_bit_cast(
                     float4, __builtin_amdgcn_raw_buffer_load_b128(rs, vo + (unsigned)(i * 32 + p * 4) * ldr4, 0, 0));
+        };
+        float4 ln_g = make_float4(0.f, 0.f, 0.f, 0.f), ln_b = ln_g;
+        __amdgpu_buffer_rsrc_t rln = rs;
+        unsigned lnld2 = 0, vln = 0x80000000u;
+        if constexpr (MODE == EPI_RESID_LN) {
+            // LN output rows through a descriptor ending at row M, like the
+            // residual; 16-bit values, four per lane.
+            if (col_ok) {
+                ln_g = *reinterpret_cast<const float4*>(epi.ln_gain + col);
+                ln_b = *reinterpret_cast<const float4*>(epi.ln_shift + col);
+            }
+            rln = __builtin_amdgcn_make_buffer_rsrc(static_cast<unsigned short*>(epi.ln_out) + wrow0 * epi.ln_ldo,
+                                                    (short)0, (int)(rows_valid * epi.ln_ldo * 2), 0x00020000);
+            lnld2 = (unsigned)epi.ln_ldo * 2u;
+            vln = col_ok ? (unsigned)rsub * lnld2 + (unsigned)col * 2u : 0x80000000u;
+        }
+        float4 hv[8];                       // EPI_RESID_LN: the pass's updated rows
+        // lnx[buf][row][wave] = (mean_w, M2_w) of the wave's columns for the
+        // pass's 32 rows, double-buffered by pass: a buffer is rewritten two
+        // passes later, after every wave has passed the barrier that follows
+        // its reads.
+        auto ln_pass = [&](int i) {
+            float2* const X = reinterpret_cast<float2*>(lnx) + (i & 1) * (32 * 8);
+            // this wave's valid columns (the tile starts at column 0: N <= 512)
+            const int nw = N - wcol0;
+            const float cnt = (float)(nw < 0 ? 0 : nw > kWN ? kWN : nw);
+#pragma unroll
+            for (int p = 0; p < 8; ++p) {
+                const float4 h = hv[p];
+                float t = col_ok ? (h.x + h.y) + (h.z + h.w) : 0.f;
+#pragma unroll
+                for (int m = 1; m < 16; m <<= 1) t += __shfl_xor(t, m, 64);
+                const float mw = cnt > 0.f ? t / cnt : 0.f;
+                float q = 0.f;
+                if (col_ok) {
+                    const float u0 = h.x - mw, u1 = h.y - mw, u2 = h.z - mw, u3 = h.w - mw;
+                    q = fmaf(u0, u0, fmaf(u1, u1, fmaf(u2, u2, u3 * u3)));
+                }
+#pragma unroll
+                for (int m = 1; m < 16; m <<= 1) q += __shfl_xor(q, m, 64);
+                if (ch == 0) X[(p * 4 + rsub) * 8 + wn] = make_float2(mw, q);
+            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            __builtin_amdgcn_s_barrier();        // every wave has written this pass's partials
+            // lane l (and l + 32) combines row l % 32
+            const float4* const xr = reinterpret_cast<const float4*>(X + lrow * 8);
+            float mean_w[8], m2_w[8];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const float4 v = xr[k];
+                mean_w[2 * k] = v.x; m2_w[2 * k] = v.y; mean_w[2 * k + 1] = v.z; m2_w[2 * k + 1] = v.w;
+            }
+            float n_w[8], tot = 0.f, sum = 0.f;
+#pragma unroll
+            for (int w = 0; w < 8; ++w) {
+                const int c = N - w * kWN;
+                n_w[w] = (float)(c < 0 ? 0 : c > kWN ? kWN : c);
+                tot += n_w[w];
+                sum = fmaf(n_w[w], mean_w[w], sum);
+            }
+            const float mu = sum / tot;
+            float M2 = 0.f;
+#pragma unroll
+            for (int w = 0; w < 8; ++w) {
+                const float dm = mean_w[w] - mu;
+                M2 += fmaf(n_w[w] * dm, dm, m2_w[w]);
+            }
+            const float rstd = 1.0f / sqrtf(M2 / tot + epi.ln_eps);
+            // LN of this lane's four columns of rows p*4 + rsub
+#pragma unroll
+            for (int p = 0; p < 8; ++p) {
+                const float mu_p = __shfl(mu, p * 4 + rsub, 64);
+                const float rs_p = __shfl(rstd, p * 4 + rsub, 64);
+                const float4 h = hv[p];
+                const unsigned lo = pack2<false>(fmaf((h.x - mu_p) * rs_p, ln_g.x, ln_b.x),
+                                                 fmaf((h.y - mu_p) * rs_p, ln_g.y, ln_b.y));
+                const unsigned hi = pack2<false>(fmaf((h.z - mu_p) * rs_p, ln_g.z, ln_b.z),
+                                                 fmaf((h.w - mu_p) * rs_p, ln_g.w, ln_b.w));
+                typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
+                __builtin_amdgcn_raw_buffer_store_b64(u32x2{lo, hi}, rln,
+                                                      vln + (unsigned)(i * 32 + p * 4) * lnld2, 0, 0);
+            }
         };
         load_resid(0, g[0]);
 #pragma unroll
@@ -183,7 +293,9 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
                                        r.z + fmaf(x[p].z, sc, bias4.z), r.w + fmaf(x[p].w, sc, bias4.w)));
                 __builtin_amdgcn_raw_buffer_store_b128(o, rs, vo + (unsigned)(i * 32 + p * 4) * ldr4, 0,
                                                        2 /* nt */);
+                if constexpr (MODE == EPI_RESID_LN) hv[p] = __builtin_bit_cast(float4, o);
             }
+            if constexpr (MODE == EPI_RESID_LN) ln_pass(i);
             __builtin_amdgcn_s_waitcnt(0xC07F);
             __builtin_amdgcn_wave_barrier();
         }
@@ -275,7 +387,7 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
         // (ch, rs) holding columns col .. col+7; the destination of row
         // wrow0 + lr0 + off is obase + off * ostride.
         const int lr0 = (rs >> 1) + 8 * (rs & 1);
-        const int rows_left = (int)min(M - wrow0 - lr0, (int64_t)kBM);
+        const int rows_left = (int)min(M - wrow0 - lr0, (int64_t)kWM);
         unsigned short* obase = static_cast<unsigned short*>(epi.out) + (wrow0 + lr0) * epi.ldo + col;
         int64_t ostride = epi.ldo;
         if constexpr (MODE == EPI_QKV_CACHE) {
@@ -342,6 +454,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
                                                            const uint8_t* __restrict__ As,
                                                            const uint8_t* __restrict__ Ws,
                                                            int64_t M, int N, int K, Epilogue epi) {
+    using SH = Shape<MODE>;
+    constexpr int kBM = SH::kBM, kBN = SH::kBN, kWavesN = SH::kWavesN;
+    constexpr int kLoadsA = SH::kLoadsA, kLoadsB = SH::kLoadsB;
     // Two LDS stages as separate arrays: the compiler can then tell that
     // fragment reads of one stage do not alias the loads filling the other.
     __shared__ __attribute__((aligned(16))) f16 sA0[kBM * kBK];
@@ -554,24 +669,43 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
     if (kt < nk) kstep(sA0, sB0, sSA0, sSB0, sA1, sB1, sSA1, sSB1, kt);
     // Past here every wave has finished its fragment reads (the trailing
     // waves' last reads precede the barrier that ended the leading waves'
-    // last step), so the stages are free for the epilogue; the leading
-    // waves' epilogue overlaps the trailing waves' last MFMAs.
+    // last step), so the stages are free for the epilogue.
 
     // ---- epilogue ------------------------------------------------------
     // Register r of transposed tile (j, i) holds output row
     // wm*128 + 32i + lane%32 and column wn*64 + 32j + 8(r/4) + 4(lane/32) + r%4.
-    const int wsel = __builtin_amdgcn_readfirstlane(wave) >> 1;
-    f16* const sbase = wsel == 0 ? sA0 : wsel == 1 ? sA1 : wsel == 2 ? sB0 : sB1;
-    char* const region = reinterpret_cast<char*>(sbase) + (wave & 1) * kRegionBytes;
-    store_tile<MODE>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane);
-    if (lead) __builtin_amdgcn_s_barrier();
+    if constexpr (SH::kWide) {
+        // The waves exchange row statistics at a workgroup barrier per pass,
+        // so the leading waves first take their pending barrier (the
+        // trailing waves' last K-step one): all eight enter the epilogue
+        // together (letting the leading waves start early measured slower).
+        // Staging regions: seven in sB0, one in sB1; the statistics go to sA0.
+        if (lead) __builtin_amdgcn_s_barrier();
+        constexpr int kRegion = 32 * kStage32 * 4;
+        char* const region = wave < 7 ? reinterpret_cast<char*>(sB0) + wave * kRegion
+                                      : reinterpret_cast<char*>(sB1);
+        store_tile<MODE>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane,
+                         reinterpret_cast<float*>(sA0), wn, lead);
+    } else {
+        const int wsel = __builtin_amdgcn_readfirstlane(wave) >> 1;
+        f16* const sbase = wsel == 0 ? sA0 : wsel == 1 ? sA1 : wsel == 2 ? sB0 : sB1;
+        char* const region = reinterpret_cast<char*>(sbase) + (wave & 1) * kRegionBytes;
+        // Epilogues writing new outputs start only after the trailing
+        // waves' last MFMAs (overlapping them measured 4-5% slower); the
+        // residual update, which reads as much as it writes, overlaps them.
+        constexpr bool kOverlap = MODE == EPI_RESID;
+        if (lead && !kOverlap) __builtin_amdgcn_s_barrier();
+        store_tile<MODE>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane, nullptr, 0, lead);
+        if (lead && kOverlap) __builtin_amdgcn_s_barrier();
+    }
 }
 
 template <int MODE, bool MX>
 hipError_t launch_mode(const void* A, int64_t lda, const void* W, const uint8_t* As,
                        const uint8_t* Ws, int64_t M, int N, int K, const Epilogue& epi,
                        hipStream_t s) {
-    const int64_t tiles = ((M + kBM - 1) / kBM) * (int64_t)((N + kBN - 1) / kBN);
+    using SH = Shape<MODE>;
+    const int64_t tiles = ((M + SH::kBM - 1) / SH::kBM) * (int64_t)((N + SH::kBN - 1) / SH::kBN);
     k_gemm_mfma<MODE, MX><<<(unsigned)tiles, kThreads, 0, s>>>(A, lda, W, As, Ws, M, N, K, epi);
     return hipGetLastError();
 }
@@ -594,6 +728,12 @@ hipError_t launch_gemm_mfma(const f16* A, int64_t lda, const f16* W, int64_t M, 
         case EPI_RESID:
             if (epi.ldr % 4 != 0) return hipErrorInvalidValue;
             return launch_mode<EPI_RESID, false>(A, lda, W, nullptr, nullptr, M, N, K, epi, s);
+        case EPI_RESID_LN:
+            static_assert(Shape<EPI_RESID_LN>::kBN == kResidLnMaxN, "tile spans the widest row");
+            if (epi.ldr % 4 != 0 || N > kResidLnMaxN || epi.ln_ldo % 4 != 0 ||
+                !epi.ln_gain || !epi.ln_shift || !epi.ln_out)
+                return hipErrorInvalidValue;
+            return launch_mode<EPI_RESID_LN, false>(A, lda, W, nullptr, nullptr, M, N, K, epi, s);
         case EPI_QKV_CACHE:
             if (epi.ldo % 8 != 0 || epi.head_dim % 8 != 0 || epi.d_model % 8 != 0)
                 return hipErrorInvalidValue;

@@ -342,29 +342,46 @@ static upr_status rank_layers_mx(const upr_model* m, const upr_kv_cache* cache,
     return UPR_OK;
 }
 
-// Attention-output projection and FFN of one layer, on the fp32 residual g:
-// g += o Wo^T + bo;  a = LN2(g);  h = gelu(a W1^T + b1);  g += h W2^T + b2.
-// Timing scopes are named "<stage>.gemm_o" etc.
+// The fp16 projection path folds each LayerNorm that follows a residual
+// update into that update's GEMM (EPI_RESID_LN) when a row fits its tile.
 template <typename Types>
-static hipError_t launch_ffn_block(const char* const names[4], const LayerWeights& w,
-                                   const typename Types::act* o, typename Types::act* a,
-                                   typename Types::act* h, float* g, int64_t R, int d, int F,
-                                   float eps, hipStream_t s) {
+static bool fused_layernorm(const upr_config& c) {
+    return std::is_same_v<Types, Bf16Types> && c.d_model <= kResidLnMaxN;
+}
+
+// Attention-output projection and FFN of one layer, on the fp32 residual g:
+// g += o Wo^T + bo;  a = LN2(g);  h = gelu(a W1^T + b1);  g += h W2^T + b2;
+// then, when next_g is given and the LayerNorm is fused, a = LN(g) with
+// (next_g, next_b).  Timing scopes are named "<stage>.gemm_o" etc.
+template <typename Types>
+static hipError_t launch_ffn_block(const char* const names[4], const upr_config& c,
+                                   const LayerWeights& w, const typename Types::act* o,
+                                   typename Types::act* a, typename Types::act* h, float* g,
+                                   int64_t R, const float* next_g, const float* next_b,
+                                   hipStream_t s) {
     using T = typename Types::kv;
     using TA = typename Types::act;
+    const int d = c.d_model, F = c.d_ff;
+    const float eps = c.ln_eps;
+    const bool fuse = fused_layernorm<Types>(c);
     hipError_t e;
     Epilogue r{};
-    r.mode = EPI_RESID;
+    r.mode = fuse ? EPI_RESID_LN : EPI_RESID;
     r.acc_scale = w.s_o;
     r.bias = w.bo;
     r.resid = g;
     r.ldr = d;
+    r.ln_gain = w.ln2_g;
+    r.ln_shift = w.ln2_b;
+    r.ln_eps = eps;
+    r.ln_out = a;
+    r.ln_ldo = d;
     {
         ProfScope ps(names[0], s);
         e = launch_gemm<TA, T>(o, d, static_cast<const TA*>(w.Wo), R, d, d, r, s);
     }
     if (e != hipSuccess) return e;
-    {
+    if (!fuse) {
         ProfScope ps(names[1], s);
         e = launch_layernorm<TA>(g, a, R, d, w.ln2_g, w.ln2_b, eps, s);
     }
@@ -380,8 +397,11 @@ static hipError_t launch_ffn_block(const char* const names[4], const LayerWeight
         e = launch_gemm<TA, T>(a, d, static_cast<const TA*>(w.W1), R, F, d, up, s);
     }
     if (e != hipSuccess) return e;
+    r.mode = fuse && next_g ? EPI_RESID_LN : EPI_RESID;
     r.acc_scale = w.s_2;
     r.bias = w.b2;
+    r.ln_gain = next_g;
+    r.ln_shift = next_b;
     ProfScope ps(names[3], s);
     return launch_gemm<TA, T>(h, F, static_cast<const TA*>(w.W2), R, d, F, r, s);
 }
@@ -416,7 +436,7 @@ static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_
                                         p.work_items, s));
     for (int l = 0; l < c.n_layers; ++l) {
         const LayerWeights& w = m->layers[l];
-        if (l > 0)
+        if (l > 0 && !fused_layernorm<Types>(c))
             UPR_LAUNCH("encode.ln1",
                        launch_layernorm<TA>(g, a, R, d, w.ln1_g, w.ln1_b, c.ln_eps, s));
         Epilogue e{};
@@ -456,7 +476,8 @@ static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_
                                                         static_cast<const T*>(e.cache_k),
                                                         static_cast<const T*>(e.cache_v),
                                                         cache->capacity_rows, s));
-        UPR_HIP(launch_ffn_block<Types>(kEncodeFfnNames, w, o, a, h, g, R, d, F, c.ln_eps, s));
+        const LayerWeights& wn = m->layers[l + 1];     // l + 1 < n_layers here
+        UPR_HIP(launch_ffn_block<Types>(kEncodeFfnNames, c, w, o, a, h, g, R, wn.ln1_g, wn.ln1_b, s));
     }
     return UPR_OK;
 }
@@ -505,7 +526,7 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
                                      p.work_items, s));
     for (int l = 0; l < c.n_layers; ++l) {
         const LayerWeights& w = m->layers[l];
-        if (l > 0)
+        if (l > 0 && !fused_layernorm<Types>(c))
             UPR_LAUNCH("rank.ln1", launch_layernorm<TA>(g, a, R, d, w.ln1_g, w.ln1_b, c.ln_eps, s));
         Epilogue e{};
         e.mode = EPI_STORE;
@@ -533,7 +554,11 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
             UPR_LAUNCH("rank.attn", launch_attn_rank_simple<T, TA>(qkv, o, R, p.row0, H, D, cand->offsets_dev,
                                                hist->offsets_dev, cand->num_users, ck, cv,
                                                cache->capacity_rows, s));
-        UPR_HIP(launch_ffn_block<Types>(kRankFfnNames, w, o, a, h, g, R, d, F, c.ln_eps, s));
+        // the next LayerNorm: layer l + 1's LN1, or LN_f before the action heads
+        const bool last = l + 1 == c.n_layers;
+        const float* ng = !last ? m->layers[l + 1].ln1_g : out.heads ? m->fin.lnf_g : nullptr;
+        const float* nb = !last ? m->layers[l + 1].ln1_b : out.heads ? m->fin.lnf_b : nullptr;
+        UPR_HIP(launch_ffn_block<Types>(kRankFfnNames, c, w, o, a, h, g, R, ng, nb, s));
     }
     }  // !mx_done
     if (!out.heads) {
@@ -545,7 +570,8 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
     // per head logit, sigmoid, utility
     const upr_heads* hd = out.heads;
     const int HC = hd->C * hd->Fh;
-    UPR_LAUNCH("rank.lnf", launch_layernorm<TA>(g, a, R, d, m->fin.lnf_g, m->fin.lnf_b, c.ln_eps, s));
+    if (mx_done || !fused_layernorm<Types>(c))
+        UPR_LAUNCH("rank.lnf", launch_layernorm<TA>(g, a, R, d, m->fin.lnf_g, m->fin.lnf_b, c.ln_eps, s));
     Epilogue e{};
     e.mode = EPI_GELU;
     e.acc_scale = hd->s_w1;

@@ -81,7 +81,13 @@ enum EpiMode : int {
                         // [2d,3d): values -> cache plane of the layer
     EPI_GELU_MX = 4,    // gelu_tanh(.) as MXFP8: E4M3 codes -> out (ldo bytes per
                         // row), one E8M0 byte per 32 columns -> out_scales
+    EPI_RESID_LN = 5,   // EPI_RESID, then ln_out[m, :] = LayerNorm(resid[m, :])
+                        // (ln_gain, ln_shift, ln_eps; projection operand type);
+                        // the tile spans whole rows, so N <= 512
 };
+
+// Widest row (N) the residual update with LayerNorm (EPI_RESID_LN) handles.
+constexpr int kResidLnMaxN = 512;
 
 struct Epilogue {
     int mode;
@@ -102,6 +108,12 @@ struct Epilogue {
     int head_dim;
     // EPI_GELU_MX: block scales, ldo / 32 bytes per row
     void* out_scales;
+    // EPI_RESID_LN: LayerNorm of the updated rows -> ln_out (leading dimension ln_ldo)
+    const float* ln_gain;
+    const float* ln_shift;
+    float ln_eps;
+    void* ln_out;
+    int64_t ln_ldo;
 };
 
 // ---------------------------------------------------------------------------

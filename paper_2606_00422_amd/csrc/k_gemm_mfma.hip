@@ -210,22 +210,38 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
             // this wave's valid columns (the tile starts at column 0: N <= 512)
             const int nw = N - wcol0;
             const float cnt = (float)(nw < 0 ? 0 : nw > kWN ? kWN : nw);
+            // Row sums over the 16 lanes of a row group, eight rows at once:
+            // each exchange halves the rows a lane keeps, so lane ch ends with
+            // row ch / 2 (8 exchanges instead of 8 x 4).
+            auto rows8_sum = [&](const float (&t)[8]) {
+                const bool b3 = ch & 8, b2 = ch & 4, b1 = ch & 2;
+                float u[4], v[2];
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    u[k] = (b3 ? t[4 + k] : t[k]) + __shfl_xor(b3 ? t[k] : t[4 + k], 8, 64);
+#pragma unroll
+                for (int k = 0; k < 2; ++k)
+                    v[k] = (b2 ? u[2 + k] : u[k]) + __shfl_xor(b2 ? u[k] : u[2 + k], 4, 64);
+                const float w = (b1 ? v[1] : v[0]) + __shfl_xor(b1 ? v[0] : v[1], 2, 64);
+                return w + __shfl_xor(w, 1, 64);
+            };
+            const int gbase = lane & ~15;
+            float t[8];
+#pragma unroll
+            for (int p = 0; p < 8; ++p) t[p] = col_ok ? (hv[p].x + hv[p].y) + (hv[p].z + hv[p].w) : 0.f;
+            const float mrow = cnt > 0.f ? rows8_sum(t) / cnt : 0.f;      // mean of row ch / 2
 #pragma unroll
             for (int p = 0; p < 8; ++p) {
-                const float4 h = hv[p];
-                float t = col_ok ? (h.x + h.y) + (h.z + h.w) : 0.f;
-#pragma unroll
-                for (int m = 1; m < 16; m <<= 1) t += __shfl_xor(t, m, 64);
-                const float mw = cnt > 0.f ? t / cnt : 0.f;
+                const float mw = __shfl(mrow, gbase + 2 * p, 64);
                 float q = 0.f;
                 if (col_ok) {
-                    const float u0 = h.x - mw, u1 = h.y - mw, u2 = h.z - mw, u3 = h.w - mw;
+                    const float u0 = hv[p].x - mw, u1 = hv[p].y - mw, u2 = hv[p].z - mw, u3 = hv[p].w - mw;
                     q = fmaf(u0, u0, fmaf(u1, u1, fmaf(u2, u2, u3 * u3)));
                 }
-#pragma unroll
-                for (int m = 1; m < 16; m <<= 1) q += __shfl_xor(q, m, 64);
-                if (ch == 0) X[(p * 4 + rsub) * 8 + wn] = make_float2(mw, q);
+                t[p] = q;
             }
+            const float qrow = rows8_sum(t);
+            if ((ch & 1) == 0) X[((ch >> 1) * 4 + rsub) * 8 + wn] = make_float2(mrow, qrow);
             __builtin_amdgcn_s_waitcnt(0xC07F);
             __builtin_amdgcn_s_barrier();        // every wave has written this pass's partials
             // lane l (and l + 32) combines row l % 32

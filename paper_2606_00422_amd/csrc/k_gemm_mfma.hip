@@ -156,11 +156,9 @@ __device__ __forceinline__ unsigned pack2(float a, float b) {
 template <int MODE>
 __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* const region,
                                            int64_t wrow0, int wcol0, int64_t M, int N,
-                                           const Epilogue& epi, int lane, float* const lnx, int wn,
-                                           bool lead) {
+                                           const Epilogue& epi, int lane, float* const lnx, int wn) {
     const int lrow = lane & 31, lhalf = lane >> 5;
     const float sc = epi.acc_scale;
-    (void)lead;
     if constexpr (MODE == EPI_RESID || MODE == EPI_RESID_LN) {
         const int ch = lane & 15, rsub = lane >> 4;
         const int col = wcol0 + ch * 4;
@@ -242,8 +240,13 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
             }
             const float qrow = rows8_sum(t);
             if ((ch & 1) == 0) X[((ch >> 1) * 4 + rsub) * 8 + wn] = make_float2(mrow, qrow);
+            // every wave has written this pass's partials (the empty asm
+            // statements keep the compiler from moving LDS accesses across
+            // the barrier)
             __builtin_amdgcn_s_waitcnt(0xC07F);
-            __builtin_amdgcn_s_barrier();        // every wave has written this pass's partials
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
             // lane l (and l + 32) combines row l % 32
             const float4* const xr = reinterpret_cast<const float4*>(X + lrow * 8);
             float mean_w[8], m2_w[8];
@@ -701,7 +704,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
         char* const region = wave < 7 ? reinterpret_cast<char*>(sB0) + wave * kRegion
                                       : reinterpret_cast<char*>(sB1);
         store_tile<MODE>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane,
-                         reinterpret_cast<float*>(sA0), wn, lead);
+                         reinterpret_cast<float*>(sA0), wn);
     } else {
         const int wsel = __builtin_amdgcn_readfirstlane(wave) >> 1;
         f16* const sbase = wsel == 0 ? sA0 : wsel == 1 ? sA1 : wsel == 2 ? sB0 : sB1;
@@ -711,7 +714,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
         // residual update, which reads as much as it writes, overlaps them.
         constexpr bool kOverlap = MODE == EPI_RESID;
         if (lead && !kOverlap) __builtin_amdgcn_s_barrier();
-        store_tile<MODE>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane, nullptr, 0, lead);
+        store_tile<MODE>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane, nullptr, 0);
         if (lead && kOverlap) __builtin_amdgcn_s_barrier();
     }
 }

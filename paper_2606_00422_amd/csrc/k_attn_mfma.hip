@@ -9,8 +9,9 @@
 // included): for history position i,  o_i = softmax([q_i . K_t]_t<=i) V.
 // Queries are pre-scaled by log2(e)/sqrt(D), so the softmax uses exp2.
 //
-// One workgroup = one work item (user, head, up to 256 query rows); four
-// waves of 64 queries.  The user's cached K/V for this layer and head are
+// One workgroup = one work item (user, head, up to 128 candidates or 256
+// history rows); four waves of 32 (ranking) or 64 (encode) queries.  The
+// user's cached K/V for this layer and head are
 // streamed through LDS in 64-key stages (double-buffered, loaded straight
 // from global memory into LDS) and shared by all queries of the item.  Per
 // 32-key sub-block each wave computes
@@ -50,10 +51,14 @@ typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 b4v;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 
 constexpr int kD = 64;            // head_dim
-constexpr int kQW = 64;           // queries per wave
-constexpr int kTQ = 4 * kQW;      // queries per work item
 constexpr int kKS = 64;           // keys per LDS stage
-static_assert(kTQ == kAttnTile, "work-list tile must match the kernel");
+// 16-query groups per wave: ranking 2 (128 VGPRs, four waves per SIMD: the
+// latency of one wave's exponentials and LDS reads hides behind three
+// others), the causal pass 4 (fewer K/V reads per query; its diagonal
+// sub-blocks are masked per wave)
+constexpr int kRankQG = 2, kEncodeQG = 4;
+static_assert(4 * 16 * kRankQG == kRankAttnTile, "ranking work-list tile must match the kernel");
+static_assert(4 * 16 * kEncodeQG == kAttnTile, "encode work-list tile must match the kernel");
 
 // LDS layout of a stage: 64 rows (keys) x 128 bytes (64 dims), the eight
 // 16-byte chunks of a row XOR-swizzled.  K fragment reads take 16
@@ -95,8 +100,8 @@ __device__ __forceinline__ float quad_sum(float v) {
 // CAUSAL = false: ranking; queries are candidate rows of qsrc = q|k|v rows
 // (stride 3d, own key and value at +d, +2d).  CAUSAL = true: encode; queries
 // are history rows of qsrc = query rows (stride d), own keys in the cache.
-template <bool CAUSAL>
-__global__ __launch_bounds__(256, 2) void k_attn_mfma(
+template <bool CAUSAL, int kQG>
+__global__ __launch_bounds__(256, 8 / kQG) void k_attn_mfma(
     const bf16* __restrict__ qsrc, int64_t qstride, f16* __restrict__ out, int64_t row0, int H,
     const int32_t* __restrict__ hist_offsets, const int4* __restrict__ work,
     const bf16* __restrict__ cache_k, const bf16* __restrict__ cache_v, int64_t cap, int force_exact) {
@@ -107,6 +112,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
     __shared__ __attribute__((aligned(16))) bf16 sV0[kKS * kD];
     __shared__ __attribute__((aligned(16))) bf16 sV1[kKS * kD];
 
+    constexpr int kQW = 16 * kQG;       // queries per wave
     const int4 item = work[blockIdx.x];
     const int u = item.x, h = item.y, kc = item.w;
     if (kc <= 0) return;
@@ -124,18 +130,18 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
     const int wave_last = ipos0 + min(wave * kQW + kQW, kc) - 1;   // encode: last query position
 
     // ---- queries of this wave (B operand of S^T), own key/value, initial state
-    b8 qf[4][2];
-    f32x4 negm[4];                      // -m of the lane's query, in all four registers
-    float l[4];                         // lane-partial sums of probabilities
-    f32x4 o[4][4];                      // O^T: e = 16eb + 4g + r of query l16
+    b8 qf[kQG][2];
+    f32x4 negm[kQG];                      // -m of the lane's query, in all four registers
+    float l[kQG];                         // lane-partial sums of probabilities
+    f32x4 o[kQG][4];                      // O^T: e = 16eb + 4g + r of query l16
     // Loads the queries and starts the softmax against reference
     // max(own logit, mref[qg]) (mref = -inf: the own logit).  Ranking starts
     // from the candidate's own key and value (p_self = 1 against its own
     // logit); encode from nothing (the diagonal key is streamed).
-    int qpos[4];                        // encode: position of the lane's query
-    auto init_state = [&](const float (&mref)[4]) __attribute__((always_inline)) {
+    int qpos[kQG];                        // encode: position of the lane's query
+    auto init_state = [&](const float (&mref)[kQG]) __attribute__((always_inline)) {
 #pragma unroll
-        for (int qg = 0; qg < 4; ++qg) {
+        for (int qg = 0; qg < kQG; ++qg) {
             int qi = wave * kQW + qg * 16 + l16;
             qi = qi < kc ? qi : kc - 1;                  // clamp the ragged tail
             qpos[qg] = ipos0 + qi;
@@ -170,7 +176,9 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
         }
     };
     {
-        const float none[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        float none[kQG];
+#pragma unroll
+        for (int qg = 0; qg < kQG; ++qg) none[qg] = -INFINITY;
         init_state(none);
     }
 
@@ -207,7 +215,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
     auto sub_block = [&](const bf16* cK, const bf16* cV, int kb, int kabs) __attribute__((always_inline)) {
         if (!wave_active || (CAUSAL && kabs > wave_last)) return;   // nothing to do for this wave
         // S^T - m for 32 keys x 64 queries
-        f32x4 s[4][2];
+        f32x4 s[kQG][2];
         // The MFMA runs of a wave take issue priority over the other wave on
         // its SIMD, whose exponentials then fill the matrix core's gaps.
         __builtin_amdgcn_s_setprio(1);
@@ -219,7 +227,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
             for (int es = 0; es < 2; ++es)
                 kf[es] = *reinterpret_cast<const b8*>(&cK[row * kD + (((es * 4 + g) ^ key_k(row)) << 3)]);
 #pragma unroll
-            for (int qg = 0; qg < 4; ++qg) {
+            for (int qg = 0; qg < kQG; ++qg) {
                 f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[0], qf[qg][0], negm[qg], 0, 0, 0);
                 s[qg][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[1], qf[qg][1], acc, 0, 0, 0);
             }
@@ -234,13 +242,13 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
                 for (int r = 0; r < 4; ++r) {
                     const int key = kabs + t * 16 + 4 * g + r;
 #pragma unroll
-                    for (int qg = 0; qg < 4; ++qg)
+                    for (int qg = 0; qg < kQG; ++qg)
                         if (CAUSAL ? key > qpos[qg] : key >= n) s[qg][t][r] = -INFINITY;
                 }
         }
-        b8 pf[4];
+        b8 pf[kQG];
 #pragma unroll
-        for (int qg = 0; qg < 4; ++qg) {
+        for (int qg = 0; qg < kQG; ++qg) {
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -270,7 +278,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
                 for (int j = 0; j < 4; ++j) vf[4 * hh + j] = v4[j];
             }
 #pragma unroll
-            for (int qg = 0; qg < 4; ++qg)
+            for (int qg = 0; qg < kQG; ++qg)
                 o[qg][eb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qg], o[qg][eb], 0, 0, 0);
         }
         __builtin_amdgcn_s_setprio(0);
@@ -306,7 +314,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
     // against it, so no probability exceeds 1.
     bool bad = force_exact != 0;
 #pragma unroll
-    for (int qg = 0; qg < 4; ++qg) {
+    for (int qg = 0; qg < kQG; ++qg) {
         bad |= nonfinite(l[qg]);
 #pragma unroll
         for (int eb = 0; eb < 4; ++eb)
@@ -314,7 +322,9 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
             for (int r = 0; r < 4; ++r) bad |= nonfinite(o[qg][eb][r]);
     }
     if (__syncthreads_or(bad)) {
-        float mref[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        float mref[kQG];
+#pragma unroll
+        for (int qg = 0; qg < kQG; ++qg) mref[qg] = -INFINITY;
         for (int st = 0; st < nst; ++st) {
             issue_loads(sK0, sV0, st);
             __builtin_amdgcn_s_waitcnt(0x0F70);
@@ -326,7 +336,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
                 for (int es = 0; es < 2; ++es)
                     kf[es] = *reinterpret_cast<const b8*>(&sK0[row * kD + (((es * 4 + g) ^ key_k(row)) << 3)]);
 #pragma unroll
-                for (int qg = 0; qg < 4; ++qg) {
+                for (int qg = 0; qg < kQG; ++qg) {
                     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
                     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[0], qf[qg][0], acc, 0, 0, 0);
                     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[1], qf[qg][1], acc, 0, 0, 0);
@@ -347,7 +357,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_mfma(
 
     // ---- normalise and store (lane holds e = 16eb + 4g + r of query l16)
 #pragma unroll
-    for (int qg = 0; qg < 4; ++qg) {
+    for (int qg = 0; qg < kQG; ++qg) {
         const int qi = wave * kQW + qg * 16 + l16;
         const float lt = quad_sum(l[qg]);
         if (qi >= kc) continue;
@@ -460,8 +470,8 @@ hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
                             int tile, const bf16* cache_k, const bf16* cache_v, int64_t cache_cap,
                             hipStream_t s) {
     if (items == 0) return hipSuccess;
-    if (D != kD || tile != kTQ) return hipErrorInvalidValue;
-    k_attn_mfma<false><<<(unsigned)items, 256, 0, s>>>(
+    if (D != kD || tile != kRankAttnTile) return hipErrorInvalidValue;
+    k_attn_mfma<false, kRankQG><<<(unsigned)items, 256, 0, s>>>(
         qkv, (int64_t)3 * H * kD, o, row0, H, hist_offsets, reinterpret_cast<const int4*>(work),
         cache_k, cache_v, cache_cap, force_exact_flag());
     return hipGetLastError();
@@ -472,8 +482,8 @@ hipError_t launch_attn_encode(const bf16* q, f16* o, int64_t row0, int H, int D,
                               int tile, const bf16* cache_k, const bf16* cache_v,
                               int64_t cache_cap, hipStream_t s) {
     if (items == 0) return hipSuccess;
-    if (D != kD || tile != kTQ) return hipErrorInvalidValue;
-    k_attn_mfma<true><<<(unsigned)items, 256, 0, s>>>(
+    if (D != kD || tile != kAttnTile) return hipErrorInvalidValue;
+    k_attn_mfma<true, kEncodeQG><<<(unsigned)items, 256, 0, s>>>(
         q, (int64_t)H * kD, o, row0, H, hist_offsets, reinterpret_cast<const int4*>(work), cache_k,
         cache_v, cache_cap, force_exact_flag());
     return hipGetLastError();

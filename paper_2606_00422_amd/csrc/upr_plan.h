@@ -12,8 +12,10 @@ namespace upr {
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // Query rows per work item of the MFMA attention (one workgroup handles this
-// many candidates, or history rows, of one user for one head).
+// many history rows, in the causal encode pass, or candidates, in ranking,
+// of one user for one head).
 constexpr int kAttnTile = 256;
+constexpr int kRankAttnTile = 128;
 constexpr bool kHaveMfmaAttn = true;
 
 struct EncodePlan {
@@ -29,7 +31,7 @@ struct RankPlan {
     int64_t row0 = 0, rows = 0;
     size_t off_g = 0, off_a = 0, off_qkv = 0, off_o = 0, off_h = 0, off_work = 0;
     int64_t work_items = 0;
-    int attn_tile = kAttnTile;
+    int attn_tile = kRankAttnTile;
     bool use_mfma_attn = false;
     size_t bytes = 0;
 };
@@ -40,10 +42,10 @@ inline bool bf16_storage(const upr_config& c) {
 inline size_t dtype_bytes(const upr_config& c) { return bf16_storage(c) ? 2 : 4; }
 
 // Number of MFMA attention work items over the rows of `offs`: one per
-// (user, head, tile of up to kAttnTile rows).
-inline int64_t attn_items(const upr_config& c, int U, const int32_t* offs) {
+// (user, head, tile of up to `tile` rows).
+inline int64_t attn_items(const upr_config& c, int U, const int32_t* offs, int tile) {
     int64_t items = 0;
-    for (int u = 0; u < U; ++u) items += ((int64_t)offs[u + 1] - offs[u] + kAttnTile - 1) / kAttnTile;
+    for (int u = 0; u < U; ++u) items += ((int64_t)offs[u + 1] - offs[u] + tile - 1) / tile;
     return items * c.n_heads;
 }
 
@@ -61,7 +63,7 @@ inline EncodePlan plan_encode(const upr_config& c, int U, const int32_t* hoffs) 
     if (p.rows <= 0) { p.rows = 0; return p; }
     const size_t es = dtype_bytes(c), R = (size_t)p.rows, d = c.d_model, F = c.d_ff;
     p.use_mfma_attn = use_mfma_attn(c);
-    if (p.use_mfma_attn) p.work_items = attn_items(c, U, hoffs);
+    if (p.use_mfma_attn) p.work_items = attn_items(c, U, hoffs, p.attn_tile);
     size_t o = 0;
     p.off_g = o; o = align256(o + R * d * 4);
     p.off_a = o; o = align256(o + R * d * es);
@@ -87,7 +89,7 @@ inline RankPlan plan_rank(const upr_config& c, int U, const int32_t* coffs, int 
     if (p.rows <= 0) { p.rows = 0; return p; }
     const size_t es = dtype_bytes(c), R = (size_t)p.rows, d = c.d_model, F = c.d_ff;
     p.use_mfma_attn = use_mfma_attn(c);
-    if (p.use_mfma_attn) p.work_items = attn_items(c, U, coffs);
+    if (p.use_mfma_attn) p.work_items = attn_items(c, U, coffs, p.attn_tile);
     size_t o = 0;
     p.off_g = o; o = align256(o + R * d * 4);
     p.off_a = o; o = align256(o + R * d * es);

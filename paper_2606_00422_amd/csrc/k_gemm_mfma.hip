@@ -68,20 +68,25 @@ typedef __attribute__((ext_vector_type(4))) int i32x4;
 
 constexpr int kBK = 64;                            // K-step (fp16 values)
 constexpr int kThreads = 512;                      // 8 waves
-constexpr int kWM = 128, kWN = 64;                 // per-wave tile
-constexpr int kTM = kWM / 32, kTN = kWN / 32;      // 32x32 MFMA tiles per wave
+constexpr int kWN = 64, kTN = kWN / 32;            // per-wave tile columns, 32-column MFMA tiles
 constexpr int kCPR = kBK / 8;                      // 16-byte chunks per LDS row (8)
-// Block tile by epilogue: 256 x 256 in a 2 (M) x 4 (N) wave grid; the
-// residual update with LayerNorm needs whole rows in one workgroup, so it
-// takes 128 x 512 with the eight waves side by side along N.  Loads per
-// leading wave per K-step: rows / 32 (a load fills 8 rows, four leading waves).
-template <int MODE>
+// Block tile by epilogue and height: 2 (M) x 4 (N) waves of (32 TM) x 64,
+// i.e. 256 x 256 for TM = 4; the residual update with LayerNorm needs whole
+// rows in one workgroup, so it takes (32 TM) x 512 with the eight waves side
+// by side along N.  TM = 4 ("tall") for large M; TM = 1 ("short") when tall
+// tiles would leave compute units idle: every output element is still the
+// same MFMA chain over K in the same order, so results do not depend on the
+// choice.  Loads per leading wave per K-step: rows / 32 (a load fills 8 rows,
+// four leading waves).
+template <int MODE, int TM>
 struct Shape {
     static constexpr bool kWide = MODE == EPI_RESID_LN;
-    static constexpr int kBM = kWide ? 128 : 256, kBN = kWide ? 512 : 256;
+    static constexpr int kTM = TM, kWM = 32 * TM;
+    static constexpr int kBM = kWide ? kWM : 2 * kWM, kBN = kWide ? 512 : 256;
     static constexpr int kWavesN = kWide ? 8 : 4;
     static constexpr int kLoadsA = kBM * kCPR / (kThreads / 2), kLoadsB = kBN * kCPR / (kThreads / 2);
 };
+
 // Epilogue staging row strides (elements).  fp32: 272 bytes, so the 16 rows
 // written by one 16-lane group of 16-byte stores fall on distinct bank
 // groups; 16-bit: 144 bytes, likewise, and rows 8 apart land on disjoint
@@ -153,10 +158,11 @@ __device__ __forceinline__ unsigned pack2(float a, float b) {
 // update: M2 = sum M2_w + n_w (mean_w - mean)^2) into the row's mean and
 // 1/sqrt(var + eps), then writes LN of its columns.  wn: the wave's column
 // block within the tile.
-template <int MODE>
+template <int MODE, int kTM>
 __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* const region,
                                            int64_t wrow0, int wcol0, int64_t M, int N,
                                            const Epilogue& epi, int lane, float* const lnx, int wn) {
+    constexpr int kWM = 32 * kTM;           // rows of the wave tile
     const int lrow = lane & 31, lhalf = lane >> 5;
     const float sc = epi.acc_scale;
     if constexpr (MODE == EPI_RESID || MODE == EPI_RESID_LN) {
@@ -467,15 +473,16 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
     }
 }
 
-template <int MODE, bool MX>
+template <int MODE, bool MX, int TM>
 __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restrict__ Av, int64_t lda,
                                                            const void* __restrict__ Wv,
                                                            const uint8_t* __restrict__ As,
                                                            const uint8_t* __restrict__ Ws,
                                                            int64_t M, int N, int K, Epilogue epi) {
-    using SH = Shape<MODE>;
+    using SH = Shape<MODE, TM>;
     constexpr int kBM = SH::kBM, kBN = SH::kBN, kWavesN = SH::kWavesN;
     constexpr int kLoadsA = SH::kLoadsA, kLoadsB = SH::kLoadsB;
+    constexpr int kTM = SH::kTM, kWM = SH::kWM;
     // Two LDS stages as separate arrays: the compiler can then tell that
     // fragment reads of one stage do not alias the loads filling the other.
     __shared__ __attribute__((aligned(16))) f16 sA0[kBM * kBK];
@@ -484,6 +491,11 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
     __shared__ __attribute__((aligned(16))) f16 sB1[kBN * kBK];
     // MXFP8: the K-step's scale dword of every row of A and of W
     __shared__ uint32_t sSA0[kBM], sSA1[kBM], sSB0[kBN], sSB1[kBN];
+    // Epilogue staging of short 256-wide tiles (their A stages are too small
+    // to hold it): one region per wave
+    constexpr int kShortRegion = 32 * kStage32 * 4;
+    constexpr bool kOwnStaging = !SH::kWide && TM < 4;
+    __shared__ __attribute__((aligned(16))) char sR[kOwnStaging ? kThreads / 64 * kShortRegion : 16];
     constexpr int kEB = MX ? 1 : 2;         // bytes per operand value
     const char* const A = static_cast<const char*>(Av);
     const char* const W = static_cast<const char*>(Wv);
@@ -509,18 +521,19 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
     // Direct global -> LDS loads by the leading waves: a load instruction's
     // 64 lanes fill 64 consecutive 16-byte LDS slots = 8 rows.  Load i of
     // leading wave lw covers rows 8 (lw kL + i) + lane/8; slot s of row r
-    // must hold logical chunk s ^ key(r), key(r) = (r / 2) % 8, which
-    // depends on i only through i % 2.  So two per-lane offsets plus a
-    // uniform step of 16 rows address every load.  (The step stays in the
-    // per-lane offset: the buffer range check that zero-fills rows past the
-    // end does not cover the scalar offset.)
+    // must hold logical chunk s ^ key(r), key(r) = (r / 2) % 8, which for
+    // loads 16 rows apart is the same.  So the offsets of a wave's first
+    // two loads plus a uniform step of 16 rows address every load (a wave
+    // with a single load, kL = 1, uses the first only).  (The step stays in
+    // the per-lane offset: the buffer range check that zero-fills rows past
+    // the end does not cover the scalar offset.)
     const int lw = wave & 3;
     int voA[2], voB[2];
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
-        const int lch = (lane & 7) ^ ((p * 4 + (lane >> 4)) & 7);
-        voA[p] = (int)(((lw * kLoadsA + p) * 8 + (lane >> 3)) * lda * kEB + lch * 16);
-        voB[p] = ((lw * kLoadsB + p) * 8 + (lane >> 3)) * K * kEB + lch * 16;
+        const int ra = (lw * kLoadsA + p) * 8 + (lane >> 3), rb = (lw * kLoadsB + p) * 8 + (lane >> 3);
+        voA[p] = (int)(ra * lda * kEB + (((lane & 7) ^ ((ra >> 1) & 7)) << 4));
+        voB[p] = rb * K * kEB + (((lane & 7) ^ ((rb >> 1) & 7)) << 4);
     }
     const int rowstepA = (int)(16 * lda * kEB), rowstepB = 16 * K * kEB;
     // MXFP8 scales: leading wave lw loads the dwords of rows 64 lw .. +63 of
@@ -532,10 +545,12 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
         (void*)(MX ? Ws + (int64_t)n0 * kblk : Ws), (short)0, MX ? (int)((int64_t)rows_b * kblk) : 0,
         0x00020000);
     const int voS = (lw * 64 + lane) * kblk;
+    static_assert(kBN == 4 * 64 || !MX, "one 64-row slice of W scales per leading wave");
     auto issue_scales = [&](uint32_t* dSA, uint32_t* dSB, int t) {
         if constexpr (MX) {
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rsSA, (__attribute__((address_space(3))) void*)(dSA + lw * 64), 4, voS + 4 * t, 0, 0, 0);
+            if (lw * 64 < kBM)      // short tiles: A has fewer rows than four slices
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rsSA, (__attribute__((address_space(3))) void*)(dSA + lw * 64), 4, voS + 4 * t, 0, 0, 0);
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
                 rsSB, (__attribute__((address_space(3))) void*)(dSB + lw * 64), 4, voS + 4 * t, 0, 0, 0);
         }
@@ -703,29 +718,55 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
         constexpr int kRegion = 32 * kStage32 * 4;
         char* const region = wave < 7 ? reinterpret_cast<char*>(sB0) + wave * kRegion
                                       : reinterpret_cast<char*>(sB1);
-        store_tile<MODE>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane,
-                         reinterpret_cast<float*>(sA0), wn);
+        store_tile<MODE, kTM>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane,
+                              reinterpret_cast<float*>(sA0), wn);
     } else {
         const int wsel = __builtin_amdgcn_readfirstlane(wave) >> 1;
         f16* const sbase = wsel == 0 ? sA0 : wsel == 1 ? sA1 : wsel == 2 ? sB0 : sB1;
-        char* const region = reinterpret_cast<char*>(sbase) + (wave & 1) * kRegionBytes;
+        char* const region = kOwnStaging ? sR + wave * kShortRegion
+                                         : reinterpret_cast<char*>(sbase) + (wave & 1) * kRegionBytes;
         // Epilogues writing new outputs start only after the trailing
         // waves' last MFMAs (overlapping them measured 4-5% slower); the
         // residual update, which reads as much as it writes, overlaps them.
         constexpr bool kOverlap = MODE == EPI_RESID;
         if (lead && !kOverlap) __builtin_amdgcn_s_barrier();
-        store_tile<MODE>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane, nullptr, 0);
+        store_tile<MODE, kTM>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane, nullptr, 0);
         if (lead && kOverlap) __builtin_amdgcn_s_barrier();
     }
+}
+
+template <int MODE, int TM>
+int64_t tile_count(int64_t M, int N) {
+    using SH = Shape<MODE, TM>;
+    return ((M + SH::kBM - 1) / SH::kBM) * (int64_t)((N + SH::kBN - 1) / SH::kBN);
+}
+
+// Compute units of the current device.
+inline int device_cus() {
+    constexpr int kMaxDevices = 64;
+    static int cached[kMaxDevices];              // 0: not yet queried
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+    if (cached[dev] == 0) {
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus <= 0)
+            return 256;
+        cached[dev] = cus;
+    }
+    return cached[dev];
 }
 
 template <int MODE, bool MX>
 hipError_t launch_mode(const void* A, int64_t lda, const void* W, const uint8_t* As,
                        const uint8_t* Ws, int64_t M, int N, int K, const Epilogue& epi,
                        hipStream_t s) {
-    using SH = Shape<MODE>;
-    const int64_t tiles = ((M + SH::kBM - 1) / SH::kBM) * (int64_t)((N + SH::kBN - 1) / SH::kBN);
-    k_gemm_mfma<MODE, MX><<<(unsigned)tiles, kThreads, 0, s>>>(A, lda, W, As, Ws, M, N, K, epi);
+    const int64_t tall = tile_count<MODE, 4>(M, N);
+    if (tall >= device_cus()) {
+        k_gemm_mfma<MODE, MX, 4><<<(unsigned)tall, kThreads, 0, s>>>(A, lda, W, As, Ws, M, N, K, epi);
+    } else {
+        const int64_t shorts = tile_count<MODE, 1>(M, N);
+        k_gemm_mfma<MODE, MX, 1><<<(unsigned)shorts, kThreads, 0, s>>>(A, lda, W, As, Ws, M, N, K, epi);
+    }
     return hipGetLastError();
 }
 
@@ -748,7 +789,7 @@ hipError_t launch_gemm_mfma(const f16* A, int64_t lda, const f16* W, int64_t M, 
             if (epi.ldr % 4 != 0) return hipErrorInvalidValue;
             return launch_mode<EPI_RESID, false>(A, lda, W, nullptr, nullptr, M, N, K, epi, s);
         case EPI_RESID_LN:
-            static_assert(Shape<EPI_RESID_LN>::kBN == kResidLnMaxN, "tile spans the widest row");
+            static_assert(Shape<EPI_RESID_LN, 4>::kBN == kResidLnMaxN, "tile spans the widest row");
             if (epi.ldr % 4 != 0 || N > kResidLnMaxN || epi.ln_ldo % 4 != 0 ||
                 !epi.ln_gain || !epi.ln_shift || !epi.ln_out)
                 return hipErrorInvalidValue;

@@ -66,6 +66,26 @@ def test_sub_range_single_user_calls_match_batch_bit_exactly():
         assert np.all(np.isnan(s[others])), "rows outside the call were written"
 
 
+def test_tile_height_does_not_change_scores():
+    """A batch large enough that every projection GEMM takes its tall tiles
+    (32768+ candidate rows at d = 256) against single-user calls, which take
+    the short tiles: each output is the same MFMA chain over K and each
+    LayerNorm row the same reduction, so the scores agree bit for bit."""
+    U, k = 16, 2100
+    inp = make_inputs([64] * U, [k] * U, 256, 4, 2, 1024, dtype="bf16", seed=33, variant="perturbed")
+    say(f"[gpu] tall vs short tiles: {U * k} candidate rows, then single users")
+    run = GpuRun(inp)
+    run.encode()
+    run.rank()
+    batch = run.scores_np().copy()
+    ho, co = inp.hist_offsets, inp.cand_offsets
+    for u in [0, 7, U - 1]:
+        run.scores.fill_(float("nan"))
+        run.rank(hoff=np.array([ho[u], ho[u + 1]], np.int32), coff=np.array([co[u], co[u + 1]], np.int32))
+        s = run.scores_np()
+        assert np.array_equal(s[co[u]:co[u + 1]], batch[co[u]:co[u + 1]]), f"user {u}"
+
+
 def test_sub_range_encode_matches_batch_encode():
     inp = _inp()
     say("[gpu] per-user encode")

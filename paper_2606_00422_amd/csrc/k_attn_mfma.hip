@@ -54,10 +54,12 @@ constexpr int kD = 64;            // head_dim
 constexpr int kKS = 64;           // keys per LDS stage
 // 16-query groups per wave: ranking 2 (128 VGPRs, four waves per SIMD: the
 // latency of one wave's exponentials and LDS reads hides behind three
-// others), the causal pass 4 (fewer K/V reads per query; its diagonal
-// sub-blocks are masked per wave)
-constexpr int kRankQG = 2, kEncodeQG = 4;
+// others), or 1 for calls too small to fill the device with 128-candidate
+// items (each query's arithmetic is the same either way); the causal pass 4
+// (fewer K/V reads per query; its diagonal sub-blocks are masked per wave)
+constexpr int kRankQG = 2, kSmallRankQG = 1, kEncodeQG = 4;
 static_assert(4 * 16 * kRankQG == kRankAttnTile, "ranking work-list tile must match the kernel");
+static_assert(4 * 16 * kSmallRankQG == kSmallRankAttnTile, "small-call tile must match the kernel");
 static_assert(4 * 16 * kEncodeQG == kAttnTile, "encode work-list tile must match the kernel");
 
 // LDS layout of a stage: 64 rows (keys) x 128 bytes (64 dims), the eight
@@ -101,7 +103,7 @@ __device__ __forceinline__ float quad_sum(float v) {
 // (stride 3d, own key and value at +d, +2d).  CAUSAL = true: encode; queries
 // are history rows of qsrc = query rows (stride d), own keys in the cache.
 template <bool CAUSAL, int kQG>
-__global__ __launch_bounds__(256, 8 / kQG) void k_attn_mfma(
+__global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
     const bf16* __restrict__ qsrc, int64_t qstride, f16* __restrict__ out, int64_t row0, int H,
     const int32_t* __restrict__ hist_offsets, const int4* __restrict__ work,
     const bf16* __restrict__ cache_k, const bf16* __restrict__ cache_v, int64_t cap, int force_exact) {
@@ -391,7 +393,8 @@ __global__ __launch_bounds__(1024) void k_rank_worklist(const int32_t* __restric
     __shared__ int s_len[kSortMax];
     __shared__ int s_tiles[kSortMax];     // tiles of the user at each rank
     __shared__ int s_user[kSortMax];      // user at each rank
-    __shared__ int s_scan[1024];
+    __shared__ int s_scan[1024];          // inclusive scan of tiles over the chunk's ranks
+    __shared__ int s_cu[1024];            // user of each rank of the chunk
     __shared__ long long s_carry;
     const int tid = threadIdx.x;
     const bool sorted = U <= kSortMax;
@@ -412,7 +415,8 @@ __global__ __launch_bounds__(1024) void k_rank_worklist(const int32_t* __restric
     }
     if (tid == 0) s_carry = 0;
     __syncthreads();
-    // chunked exclusive scan of tiles in rank order; each rank then writes its items
+    // chunked scan of tiles in rank order; the chunk's items are then written
+    // by all threads, each finding its tile's rank by binary search
     for (int base = 0; base < U; base += 1024) {
         const int r = base + tid;
         int u = -1, t = 0;
@@ -428,21 +432,30 @@ __global__ __launch_bounds__(1024) void k_rank_worklist(const int32_t* __restric
             s_scan[tid] += v;
             __syncthreads();
         }
-        const long long start = s_carry + s_scan[tid] - t;
-        if (u >= 0) {
-            const int k = coffs[u + 1] - coffs[u];
-            for (int j = 0; j < t; ++j)
-                for (int hh = 0; hh < H; ++hh) {
-                    const long long idx = (long long)H * (start + j) + hh;
-                    if (idx < items) {
-                        const int tt = reverse ? t - 1 - j : j;
-                        const int cnt = min(tile, k - tt * tile);
-                        work[idx] = make_int4(u, hh, coffs[u] + tt * tile, cnt);
-                    }
-                }
+        s_cu[tid] = u;
+        __syncthreads();
+        const int total = s_scan[1023];                 // tiles of this chunk
+        const int nr = min(1024, U - base);             // ranks of this chunk
+        for (long long it = tid; it < (long long)total * H; it += 1024) {
+            const int x = (int)(it / H), hh = (int)(it % H);
+            int lo = 0, hi = nr - 1;                    // smallest rank with s_scan > x
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (s_scan[mid] > x) hi = mid; else lo = mid + 1;
+            }
+            const int ur = s_cu[lo];
+            const int tr = s_scan[lo] - (lo > 0 ? s_scan[lo - 1] : 0);
+            const int j = x - (s_scan[lo] - tr);
+            const long long idx = (long long)H * (s_carry + x) + hh;
+            if (idx < items) {
+                const int k = coffs[ur + 1] - coffs[ur];
+                const int tt = reverse ? tr - 1 - j : j;
+                const int cnt = min(tile, k - tt * tile);
+                work[idx] = make_int4(ur, hh, coffs[ur] + tt * tile, cnt);
+            }
         }
         __syncthreads();
-        if (tid == 1023) s_carry += s_scan[1023];
+        if (tid == 1023) s_carry += total;
         __syncthreads();
     }
 }
@@ -470,10 +483,15 @@ hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
                             int tile, const bf16* cache_k, const bf16* cache_v, int64_t cache_cap,
                             hipStream_t s) {
     if (items == 0) return hipSuccess;
-    if (D != kD || tile != kRankAttnTile) return hipErrorInvalidValue;
-    k_attn_mfma<false, kRankQG><<<(unsigned)items, 256, 0, s>>>(
-        qkv, (int64_t)3 * H * kD, o, row0, H, hist_offsets, reinterpret_cast<const int4*>(work),
-        cache_k, cache_v, cache_cap, force_exact_flag());
+    if (D != kD || (tile != kRankAttnTile && tile != kSmallRankAttnTile)) return hipErrorInvalidValue;
+    if (tile == kRankAttnTile)
+        k_attn_mfma<false, kRankQG><<<(unsigned)items, 256, 0, s>>>(
+            qkv, (int64_t)3 * H * kD, o, row0, H, hist_offsets, reinterpret_cast<const int4*>(work),
+            cache_k, cache_v, cache_cap, force_exact_flag());
+    else
+        k_attn_mfma<false, kSmallRankQG><<<(unsigned)items, 256, 0, s>>>(
+            qkv, (int64_t)3 * H * kD, o, row0, H, hist_offsets, reinterpret_cast<const int4*>(work),
+            cache_k, cache_v, cache_cap, force_exact_flag());
     return hipGetLastError();
 }
 

@@ -16,6 +16,8 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 // of one user for one head).
 constexpr int kAttnTile = 256;
 constexpr int kRankAttnTile = 128;
+constexpr int kSmallRankAttnTile = 64;      // ranking calls with few work items
+constexpr int64_t kSmallRankItems = 512;    // fewer 128-candidate items than this
 constexpr bool kHaveMfmaAttn = true;
 
 struct EncodePlan {
@@ -89,7 +91,13 @@ inline RankPlan plan_rank(const upr_config& c, int U, const int32_t* coffs, int 
     if (p.rows <= 0) { p.rows = 0; return p; }
     const size_t es = dtype_bytes(c), R = (size_t)p.rows, d = c.d_model, F = c.d_ff;
     p.use_mfma_attn = use_mfma_attn(c);
-    if (p.use_mfma_attn) p.work_items = attn_items(c, U, coffs, p.attn_tile);
+    if (p.use_mfma_attn) {
+        p.work_items = attn_items(c, U, coffs, p.attn_tile);
+        if (p.work_items < kSmallRankItems) {
+            p.attn_tile = kSmallRankAttnTile;
+            p.work_items = attn_items(c, U, coffs, p.attn_tile);
+        }
+    }
     size_t o = 0;
     p.off_g = o; o = align256(o + R * d * 4);
     p.off_a = o; o = align256(o + R * d * es);

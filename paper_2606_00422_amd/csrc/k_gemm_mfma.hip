@@ -329,8 +329,13 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
         // the 32 columns of block j (8q + 4h .. +3, q = 0..3) and lane l^32
         // the other sixteen: one exchange gives the block maximum.  After
         // encoding, two v_permlane32_swap exchanges give lane l (h = 0) the
-        // codes of columns 0-15 and lane l+32 those of 16-31, so each writes
-        // 16 consecutive bytes; lanes of h = 0 write the row's two scale bytes.
+        // codes of columns 0-15 and lane l+32 those of 16-31; lanes of h = 0
+        // write the row's two scale bytes.  The codes are staged through the
+        // wave's LDS region (32 rows x 80 bytes: 16-byte writes of 16
+        // consecutive rows fall on distinct bank groups) and written back as
+        // the row's whole 64 bytes, 16 rows per store instruction (stores
+        // straight from the MFMA layout cover 32 bytes of 32 rows and doubled
+        // the HBM write traffic).
         float4 bq[kTN][4];
 #pragma unroll
         for (int j = 0; j < kTN; ++j)
@@ -342,6 +347,8 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
             }
         uint8_t* const codes = static_cast<uint8_t*>(epi.out);
         uint8_t* const scales = static_cast<uint8_t*>(epi.out_scales);
+        unsigned char* const stg = reinterpret_cast<unsigned char*>(region);
+        constexpr int kStageMx = 80;            // staging row stride (bytes)
         const int64_t lds = epi.ldo / kMxBlock;
         const bool cols_ok = wcol0 < N;                 // N is a multiple of 64
 #pragma unroll
@@ -373,13 +380,23 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
                 const auto r13 = __builtin_amdgcn_permlane32_swap(u[1], u[3], false, false);
                 const u32x4 o = {r02[0], r02[1], r13[0], r13[1]};
                 sc2 |= (unsigned)(e + 127) << (8 * j);
-                if (row < M && cols_ok)
-                    __builtin_nontemporal_store(
-                        o, reinterpret_cast<u32x4*>(codes + row * epi.ldo + wcol0 + j * 32 + 16 * lhalf));
+                *reinterpret_cast<u32x4*>(stg + lrow * kStageMx + j * 32 + 16 * lhalf) = o;
             }
             if (lhalf == 0 && row < M && cols_ok)
                 *reinterpret_cast<unsigned short*>(scales + row * lds + wcol0 / kMxBlock) =
                     (unsigned short)sc2;
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int pp = 0; pp < 2; ++pp) {
+                const int r = pp * 16 + (lane >> 2), c = (lane & 3) * 16;
+                const u32x4 x = *reinterpret_cast<const u32x4*>(stg + r * kStageMx + c);
+                const int64_t grow = wrow0 + i * 32 + r;
+                if (grow < M && cols_ok)
+                    __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(codes + grow * epi.ldo + wcol0 + c));
+            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            __builtin_amdgcn_wave_barrier();
         }
     } else {
         // Per run of four columns: multiplier and bias.  EPI_STORE scales

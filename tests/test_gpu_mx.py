@@ -151,3 +151,45 @@ def test_mxfp8_headline_workload_sampled():
                         inp.cand_emb, inp.cand_offsets, users=users, cand_rows=rows)
     _check_mx_scores(g[rows], o[rows], exact[rows], "headline sample")
     assert np.all(np.isfinite(g[: int(run.coff[-1])]))
+
+
+def test_mxfp8_action_heads_follow_the_rule():
+    """Per-action heads on a UPR_BF16_MXFP8 model: the heads themselves keep
+    the bf16 model's precision, so the probabilities move with the fp8
+    hidden state only.  Held to the same relative envelope as the scores:
+    closer to the oracle's fp8 rule than the rule is to the exact model,
+    visibly away from the exact model, correlated; top-K is exact on the
+    GPU's own utilities."""
+    from synth import make_heads
+    from tests.test_gpu_heads import _check_topk, _run_actions
+    hl, kl, d, H, L, F = CASES[0]
+    C, Fh = 3, 64
+    inp = make_inputs(hl, kl, d, H, L, F, dtype="bf16", seed=410, variant="perturbed")
+    hb = make_heads(d, C, Fh, dtype="bf16", seed=411, variant="perturbed")
+    uw = np.array([1.0, 0.5, -2.0], dtype=np.float32)
+    say(f"[gpu] mxfp8 heads: U={inp.U} Kc={inp.cand_offsets[-1]} d={d} C={C} Fh={Fh}")
+    run = GpuRun(inp, model_dtype="bf16_mxfp8")
+    run.encode()
+    g_probs, g_util = _run_actions(run, hb, C, Fh, uw)
+    _, final = oracle.unpack_weights(inp.weights, d, L, F)
+    cache = oracle.encode(inp.weights, d, H, L, F, inp.hist_emb, inp.hist_offsets)
+
+    def probs(proj):
+        hid = oracle.rank_hidden(inp.weights, d, H, L, F, cache, inp.hist_offsets, inp.cand_emb,
+                                 inp.cand_offsets, proj=proj)
+        return oracle.sigmoid(oracle.action_logits(hid, final, hb, d, C, Fh))
+
+    rule, exact = probs("mxfp8"), probs("exact")
+    rows = int(inp.cand_offsets[-1])
+    ok = ~np.isnan(rule[:rows]).any(axis=1)
+    g, rule, exact = g_probs[:rows][ok].ravel(), rule[:rows][ok].ravel(), exact[:rows][ok].ravel()
+    assert np.all(np.isfinite(g))
+    rms = lambda v: float(np.sqrt(np.mean(v ** 2)))
+    d_rule, d_exact, d_own = rms(g - rule), rms(g - exact), rms(rule - exact)
+    corr = float(np.corrcoef(g, rule)[0, 1])
+    say(f"[gpu]   rms(gpu-rule) {d_rule:.3e}, rms(rule-exact) {d_own:.3e}, rms(gpu-exact) {d_exact:.3e}, "
+        f"corr {corr:.5f}, max {np.abs(g - rule).max():.3e}")
+    assert d_rule < 0.8 * d_own and d_exact > 0.5 * d_own and corr >= MX_CORR
+    assert np.abs(g - rule).max() <= 0.25 * MX_MAX      # sigmoid slope <= 1/4
+    for K in (1, 5, 64):
+        _check_topk(run, g_util[: max(rows, 1)], K)

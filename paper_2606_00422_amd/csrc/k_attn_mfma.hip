@@ -37,6 +37,7 @@
 // is redone exactly: a first pass finds each query's maximum logit, and the
 // second runs against it.  Row sums use v_dot2 over the bf16 probabilities,
 // the same values that weight V.
+#include "mx.h"
 #include "upr_plan.h"
 
 #include <cstdlib>
@@ -102,9 +103,12 @@ __device__ __forceinline__ float quad_sum(float v) {
 // CAUSAL = false: ranking; queries are candidate rows of qsrc = q|k|v rows
 // (stride 3d, own key and value at +d, +2d).  CAUSAL = true: encode; queries
 // are history rows of qsrc = query rows (stride d), own keys in the cache.
-template <bool CAUSAL, int kQG>
+// MXO: the output goes out as MXFP8 (codes in `out`, one E8M0 byte per
+// 32-value block in `out_scales`) for the fp8 projection variant; else fp16.
+template <bool CAUSAL, int kQG, bool MXO = false>
 __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
-    const bf16* __restrict__ qsrc, int64_t qstride, f16* __restrict__ out, int64_t row0, int H,
+    const bf16* __restrict__ qsrc, int64_t qstride, void* __restrict__ out,
+    uint8_t* __restrict__ out_scales, int64_t row0, int H,
     const int32_t* __restrict__ hist_offsets, const int4* __restrict__ work,
     const bf16* __restrict__ cache_k, const bf16* __restrict__ cache_v, int64_t cap, int force_exact) {
     // Stages as separate arrays: the compiler can then tell that reads of one
@@ -362,16 +366,44 @@ __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
     for (int qg = 0; qg < kQG; ++qg) {
         const int qi = wave * kQW + qg * 16 + l16;
         const float lt = quad_sum(l[qg]);
-        if (qi >= kc) continue;
         const float inv = 1.0f / lt;
-        f16* orow = out + (c0 - row0 + qi) * (int64_t)d + h * kD;
+        const int64_t orow = c0 - row0 + qi;
+        if constexpr (!MXO) {
+            if (qi >= kc) continue;
+            f16* op = static_cast<f16*>(out) + orow * d + h * kD;
 #pragma unroll
-        for (int eb = 0; eb < 4; ++eb) {
-            typedef __attribute__((ext_vector_type(4))) _Float16 h4;
-            h4 v;
+            for (int eb = 0; eb < 4; ++eb) {
+                typedef __attribute__((ext_vector_type(4))) _Float16 h4;
+                h4 v;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = (f16)keep_f32(o[qg][eb][r] * inv);
-            *reinterpret_cast<h4*>(orow + eb * 16 + 4 * g) = v;
+                for (int r = 0; r < 4; ++r) v[r] = (f16)keep_f32(o[qg][eb][r] * inv);
+                *reinterpret_cast<h4*>(op + eb * 16 + 4 * g) = v;
+            }
+        } else {
+            // The fp16 values the unfused path stores, then encoded as the
+            // standalone MXFP8 encoder would encode them: a head's 64 values
+            // are blocks 2h and 2h + 1 of the row (e < 32 and e >= 32, i.e.
+            // eb < 2 and eb >= 2), each spread over the query's four lanes.
+            float am[2] = {0.f, 0.f};
+#pragma unroll
+            for (int eb = 0; eb < 4; ++eb)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    o[qg][eb][r] = (float)(f16)keep_f32(o[qg][eb][r] * inv);
+                    am[eb >> 1] = fmaxf(am[eb >> 1], fabsf(o[qg][eb][r]));
+                }
+#pragma unroll
+            for (int b = 0; b < 2; ++b) am[b] = pair_max32(pair_max16(am[b]));
+            if (qi >= kc) continue;
+            const int e[2] = {mx_block_exp(am[0]), mx_block_exp(am[1])};
+            uint8_t* cp = static_cast<uint8_t*>(out) + orow * d + h * kD;
+#pragma unroll
+            for (int eb = 0; eb < 4; ++eb) {
+                const float sc = mx_inv_scale(e[eb >> 1]);
+                *reinterpret_cast<uint32_t*>(cp + eb * 16 + 4 * g) =
+                    mx_pack4(o[qg][eb][0] * sc, o[qg][eb][1] * sc, o[qg][eb][2] * sc, o[qg][eb][3] * sc);
+            }
+            if (g < 2) out_scales[orow * (d / kMxBlock) + h * (kD / kMxBlock) + g] = (uint8_t)(e[g] + 127);
         }
     }
 }
@@ -486,12 +518,30 @@ hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
     if (D != kD || (tile != kRankAttnTile && tile != kSmallRankAttnTile)) return hipErrorInvalidValue;
     if (tile == kRankAttnTile)
         k_attn_mfma<false, kRankQG><<<(unsigned)items, 256, 0, s>>>(
-            qkv, (int64_t)3 * H * kD, o, row0, H, hist_offsets, reinterpret_cast<const int4*>(work),
-            cache_k, cache_v, cache_cap, force_exact_flag());
+            qkv, (int64_t)3 * H * kD, o, nullptr, row0, H, hist_offsets,
+            reinterpret_cast<const int4*>(work), cache_k, cache_v, cache_cap, force_exact_flag());
     else
         k_attn_mfma<false, kSmallRankQG><<<(unsigned)items, 256, 0, s>>>(
-            qkv, (int64_t)3 * H * kD, o, row0, H, hist_offsets, reinterpret_cast<const int4*>(work),
-            cache_k, cache_v, cache_cap, force_exact_flag());
+            qkv, (int64_t)3 * H * kD, o, nullptr, row0, H, hist_offsets,
+            reinterpret_cast<const int4*>(work), cache_k, cache_v, cache_cap, force_exact_flag());
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_rank_mx(const bf16* qkv, uint8_t* codes, uint8_t* scales, int64_t row0,
+                               int H, int D, const int32_t* hist_offsets, const int32_t* work,
+                               int64_t items, int tile, const bf16* cache_k, const bf16* cache_v,
+                               int64_t cache_cap, hipStream_t s) {
+    if (items == 0) return hipSuccess;
+    if (D != kD || (tile != kRankAttnTile && tile != kSmallRankAttnTile) || scales == nullptr)
+        return hipErrorInvalidValue;
+    if (tile == kRankAttnTile)
+        k_attn_mfma<false, kRankQG, true><<<(unsigned)items, 256, 0, s>>>(
+            qkv, (int64_t)3 * H * kD, codes, scales, row0, H, hist_offsets,
+            reinterpret_cast<const int4*>(work), cache_k, cache_v, cache_cap, force_exact_flag());
+    else
+        k_attn_mfma<false, kSmallRankQG, true><<<(unsigned)items, 256, 0, s>>>(
+            qkv, (int64_t)3 * H * kD, codes, scales, row0, H, hist_offsets,
+            reinterpret_cast<const int4*>(work), cache_k, cache_v, cache_cap, force_exact_flag());
     return hipGetLastError();
 }
 
@@ -502,7 +552,7 @@ hipError_t launch_attn_encode(const bf16* q, f16* o, int64_t row0, int H, int D,
     if (items == 0) return hipSuccess;
     if (D != kD || tile != kAttnTile) return hipErrorInvalidValue;
     k_attn_mfma<true, kEncodeQG><<<(unsigned)items, 256, 0, s>>>(
-        q, (int64_t)H * kD, o, row0, H, hist_offsets, reinterpret_cast<const int4*>(work), cache_k,
+        q, (int64_t)H * kD, o, nullptr, row0, H, hist_offsets, reinterpret_cast<const int4*>(work), cache_k,
         cache_v, cache_cap, force_exact_flag());
     return hipGetLastError();
 }

@@ -268,8 +268,8 @@ void mx_quantize_host(const float* x, int64_t rows, int k, uint8_t* codes, uint8
 
 // Candidate layers of the fp8-projection variant: the bf16 sequence with
 // MXFP8 projection operands (LayerNorms write MXFP8 directly, the attention
-// output is encoded from fp16, the FFN-up GEMM writes its GELU output as
-// MXFP8).
+// kernel encodes its fp16-rounded output, the FFN-up GEMM writes its GELU
+// output as MXFP8).
 static upr_status rank_layers_mx(const upr_model* m, const upr_kv_cache* cache,
                                  const upr_segments* hist, const bf16* cand_emb,
                                  const upr_segments* cand, const RankPlan& p, char* ws,
@@ -309,17 +309,19 @@ static upr_status rank_layers_mx(const upr_model* m, const upr_kv_cache* cache,
         UPR_LAUNCH("rank.gemm_qkv", launch_gemm_mx(ac, asc, w.mx_qkv, w.mx_qkv_s, R, 3 * d, d, e, s));
         const bf16* ck = static_cast<const bf16*>(plane_ptr(c, cache, l, 0));
         const bf16* cv = static_cast<const bf16*>(plane_ptr(c, cache, l, 1));
-        if (p.use_mfma_attn)
-            UPR_LAUNCH("rank.attn", launch_attn_rank(qkv, o, p.row0, H, D, hist->offsets_dev,
-                                                     reinterpret_cast<const int32_t*>(ws + p.off_work),
-                                                     p.work_items, p.attn_tile, ck, cv,
-                                                     cache->capacity_rows, s));
-        else
+        if (p.use_mfma_attn) {
+            // attention writes the O projection's MXFP8 operand directly
+            UPR_LAUNCH("rank.attn", launch_attn_rank_mx(qkv, ac, asc, p.row0, H, D, hist->offsets_dev,
+                                                        reinterpret_cast<const int32_t*>(ws + p.off_work),
+                                                        p.work_items, p.attn_tile, ck, cv,
+                                                        cache->capacity_rows, s));
+        } else {
             UPR_LAUNCH("rank.attn",
                        launch_attn_rank_simple<bf16, f16>(qkv, o, R, p.row0, H, D, cand->offsets_dev,
                                                           hist->offsets_dev, cand->num_users, ck, cv,
                                                           cache->capacity_rows, s));
-        UPR_LAUNCH("rank.quant_o", launch_mx_quantize<f16>(o, R, d, ac, asc, s));
+            UPR_LAUNCH("rank.quant_o", launch_mx_quantize<f16>(o, R, d, ac, asc, s));
+        }
         Epilogue r{};
         r.mode = EPI_RESID;
         r.acc_scale = 1.0f;

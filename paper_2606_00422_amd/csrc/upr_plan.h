@@ -134,6 +134,14 @@ hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
                             int tile, const bf16* cache_k, const bf16* cache_v, int64_t cache_cap,
                             hipStream_t s);
 
+// The same with the output as MXFP8 (codes [rows, H*64], one E8M0 scale byte
+// per 32-value block [rows, H*2]), encoded from the fp16 values the call
+// above writes: the fp8 projection variant's input of the O projection.
+hipError_t launch_attn_rank_mx(const bf16* qkv, uint8_t* codes, uint8_t* scales, int64_t row0,
+                               int H, int D, const int32_t* hist_offsets, const int32_t* work,
+                               int64_t items, int tile, const bf16* cache_k, const bf16* cache_v,
+                               int64_t cache_cap, hipStream_t s);
+
 // MFMA causal encode attention (bf16 query rows and cache, head_dim 64),
 // fp16 output.
 hipError_t launch_attn_encode(const bf16* q, f16* o, int64_t row0, int H, int D,

@@ -1,6 +1,6 @@
-// MXFP8 encoding of row-major activations (fp8 projection variant: the
-// attention output before the output projection, and the library's
-// upr_mx_quantize call).
+// MXFP8 encoding of row-major activations (the library's upr_mx_quantize
+// call, and the fp8 projection variant's attention output when the
+// reference attention kernel computed it).
 //
 // One wave per row.  A lane takes eight consecutive values per 512-value
 // stretch of the row, so one 32-value block is four consecutive lanes: the

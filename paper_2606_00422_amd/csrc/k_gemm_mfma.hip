@@ -33,7 +33,10 @@
 // pass of the residual update, each wave reduces per-row mean and squared
 // deviations over its columns, the waves exchange them through LDS at a
 // workgroup barrier, and each writes the normalized values of its columns as
-// fp16: the updated residual is never read back from HBM.
+// fp16: the updated residual is never read back from HBM.  With MXFP8
+// operands (EPI_RESID_LN_MX) the LayerNorm is written as MXFP8 (a 32-column
+// block is eight lanes of a row group) and the tile is 64 x 512: two
+// 128-row stages would leave no LDS for the K-step's scale dwords.
 //
 // Tile order is XCD-aware: workgroup b runs on XCD b % 8 and the tiles are
 // renumbered so each XCD sweeps a contiguous range of (M-panel, N-tile)
@@ -80,7 +83,7 @@ constexpr int kCPR = kBK / 8;                      // 16-byte chunks per LDS row
 // four leading waves).
 template <int MODE, int TM>
 struct Shape {
-    static constexpr bool kWide = MODE == EPI_RESID_LN;
+    static constexpr bool kWide = MODE == EPI_RESID_LN || MODE == EPI_RESID_LN_MX;
     static constexpr int kTM = TM, kWM = 32 * TM;
     static constexpr int kBM = kWide ? kWM : 2 * kWM, kBN = kWide ? 512 : 256;
     static constexpr int kWavesN = kWide ? 8 : 4;
@@ -165,7 +168,8 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
     constexpr int kWM = 32 * kTM;           // rows of the wave tile
     const int lrow = lane & 31, lhalf = lane >> 5;
     const float sc = epi.acc_scale;
-    if constexpr (MODE == EPI_RESID || MODE == EPI_RESID_LN) {
+    if constexpr (MODE == EPI_RESID || MODE == EPI_RESID_LN || MODE == EPI_RESID_LN_MX) {
+        constexpr bool kLN = MODE != EPI_RESID, kLnMx = MODE == EPI_RESID_LN_MX;
         const int ch = lane & 15, rsub = lane >> 4;
         const int col = wcol0 + ch * 4;
         const bool col_ok = col < N;                  // N is a multiple of 8
@@ -190,19 +194,28 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
                     float4, __builtin_amdgcn_raw_buffer_load_b128(rs, vo + (unsigned)(i * 32 + p * 4) * ldr4, 0, 0));
         };
         float4 ln_g = make_float4(0.f, 0.f, 0.f, 0.f), ln_b = ln_g;
-        __amdgpu_buffer_rsrc_t rln = rs;
-        unsigned lnld2 = 0, vln = 0x80000000u;
-        if constexpr (MODE == EPI_RESID_LN) {
+        __amdgpu_buffer_rsrc_t rln = rs, rlns = rs;
+        unsigned lnld2 = 0, vln = 0x80000000u, lnsld = 0, vlns = 0x80000000u;
+        if constexpr (kLN) {
             // LN output rows through a descriptor ending at row M, like the
-            // residual; 16-bit values, four per lane.
+            // residual; 16-bit values, or MXFP8 codes (and a second
+            // descriptor over the scale bytes), four per lane.
+            constexpr int kOB = kLnMx ? 1 : 2;      // bytes per output value
             if (col_ok) {
                 ln_g = *reinterpret_cast<const float4*>(epi.ln_gain + col);
                 ln_b = *reinterpret_cast<const float4*>(epi.ln_shift + col);
             }
-            rln = __builtin_amdgcn_make_buffer_rsrc(static_cast<unsigned short*>(epi.ln_out) + wrow0 * epi.ln_ldo,
-                                                    (short)0, (int)(rows_valid * epi.ln_ldo * 2), 0x00020000);
-            lnld2 = (unsigned)epi.ln_ldo * 2u;
-            vln = col_ok ? (unsigned)rsub * lnld2 + (unsigned)col * 2u : 0x80000000u;
+            rln = __builtin_amdgcn_make_buffer_rsrc(static_cast<char*>(epi.ln_out) + wrow0 * epi.ln_ldo * kOB,
+                                                    (short)0, (int)(rows_valid * epi.ln_ldo * kOB), 0x00020000);
+            lnld2 = (unsigned)epi.ln_ldo * kOB;
+            vln = col_ok ? (unsigned)rsub * lnld2 + (unsigned)col * kOB : 0x80000000u;
+            if constexpr (kLnMx) {
+                const int64_t sld = epi.ln_ldo / kMxBlock;
+                rlns = __builtin_amdgcn_make_buffer_rsrc(static_cast<char*>(epi.ln_scales) + wrow0 * sld,
+                                                         (short)0, (int)(rows_valid * sld), 0x00020000);
+                lnsld = (unsigned)sld;
+                vlns = col_ok ? (unsigned)rsub * lnsld + (unsigned)(wcol0 / kMxBlock) : 0x80000000u;
+            }
         }
         float4 hv[8];                       // EPI_RESID_LN: the pass's updated rows
         // lnx[buf][row][wave] = (mean_w, M2_w) of the wave's columns for the
@@ -283,6 +296,30 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
                 const float mu_p = __shfl(mu, p * 4 + rsub, 64);
                 const float rs_p = __shfl(rstd, p * 4 + rsub, 64);
                 const float4 h = hv[p];
+                if constexpr (kLnMx) {
+                    // a 32-column block is eight lanes (ch 0-7 or 8-15 of
+                    // the row group); its first lane's pair of lanes writes
+                    // the wave's two scale bytes
+                    float y[4] = {keep_f32(fmaf((h.x - mu_p) * rs_p, ln_g.x, ln_b.x)),
+                                  keep_f32(fmaf((h.y - mu_p) * rs_p, ln_g.y, ln_b.y)),
+                                  keep_f32(fmaf((h.z - mu_p) * rs_p, ln_g.z, ln_b.z)),
+                                  keep_f32(fmaf((h.w - mu_p) * rs_p, ln_g.w, ln_b.w))};
+                    if (!col_ok) y[0] = y[1] = y[2] = y[3] = 0.f;
+                    float amax = fmaxf(fmaxf(fabsf(y[0]), fabsf(y[1])), fmaxf(fabsf(y[2]), fabsf(y[3])));
+                    amax = fmaxf(amax, __shfl_xor(amax, 1, 64));
+                    amax = fmaxf(amax, __shfl_xor(amax, 2, 64));
+                    amax = fmaxf(amax, __shfl_xor(amax, 4, 64));
+                    const int e = mx_block_exp(amax);
+                    const float inv = mx_inv_scale(e);
+                    __builtin_amdgcn_raw_buffer_store_b32(mx_pack4(y[0] * inv, y[1] * inv, y[2] * inv, y[3] * inv),
+                                                          rln, vln + (unsigned)(i * 32 + p * 4) * lnld2, 0, 0);
+                    const int e_hi = __shfl_xor(e, 8, 64);
+                    if (ch == 0)
+                        __builtin_amdgcn_raw_buffer_store_b16(
+                            (unsigned short)((e + 127) | ((e_hi + 127) << 8)), rlns,
+                            vlns + (unsigned)(i * 32 + p * 4) * lnsld, 0, 0);
+                    continue;
+                }
                 const unsigned lo = pack2<false>(fmaf((h.x - mu_p) * rs_p, ln_g.x, ln_b.x),
                                                  fmaf((h.y - mu_p) * rs_p, ln_g.y, ln_b.y));
                 const unsigned hi = pack2<false>(fmaf((h.z - mu_p) * rs_p, ln_g.z, ln_b.z),
@@ -318,9 +355,9 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
                                        r.z + fmaf(x[p].z, sc, bias4.z), r.w + fmaf(x[p].w, sc, bias4.w)));
                 __builtin_amdgcn_raw_buffer_store_b128(o, rs, vo + (unsigned)(i * 32 + p * 4) * ldr4, 0,
                                                        2 /* nt */);
-                if constexpr (MODE == EPI_RESID_LN) hv[p] = __builtin_bit_cast(float4, o);
+                if constexpr (kLN) hv[p] = __builtin_bit_cast(float4, o);
             }
-            if constexpr (MODE == EPI_RESID_LN) ln_pass(i);
+            if constexpr (kLN) ln_pass(i);
             __builtin_amdgcn_s_waitcnt(0xC07F);
             __builtin_amdgcn_wave_barrier();
         }
@@ -507,7 +544,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
     __shared__ __attribute__((aligned(16))) f16 sB0[kBN * kBK];
     __shared__ __attribute__((aligned(16))) f16 sB1[kBN * kBK];
     // MXFP8: the K-step's scale dword of every row of A and of W
-    __shared__ uint32_t sSA0[kBM], sSA1[kBM], sSB0[kBN], sSB1[kBN];
+    // (at least one 64-row slice each: a slice is one load instruction)
+    constexpr int kSA = MX ? (kBM < 64 ? 64 : kBM) : 1, kSB = MX ? kBN : 1;
+    __shared__ uint32_t sSA0[kSA], sSA1[kSA], sSB0[kSB], sSB1[kSB];
     // Epilogue staging of short 256-wide tiles (their A stages are too small
     // to hold it): one region per wave
     constexpr int kShortRegion = 32 * kStage32 * 4;
@@ -553,8 +592,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
         voB[p] = rb * K * kEB + (((lane & 7) ^ ((rb >> 1) & 7)) << 4);
     }
     const int rowstepA = (int)(16 * lda * kEB), rowstepB = 16 * K * kEB;
-    // MXFP8 scales: leading wave lw loads the dwords of rows 64 lw .. +63 of
-    // A and of W for a K-step (K/32 bytes per row; dword t = blocks 4t..4t+3)
+    // MXFP8 scales: leading wave lw loads the dwords of rows 64 (lw + 4 s)
+    // .. +63, s = 0, 1, .., of A and of W for a K-step (K/32 bytes per row;
+    // dword t = blocks 4t..4t+3)
     const int kblk = K / kMxBlock;
     const __amdgpu_buffer_rsrc_t rsSA = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(MX ? As + m0 * kblk : As), (short)0, MX ? (int)(rows_a * kblk) : 0, 0x00020000);
@@ -562,14 +602,23 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
         (void*)(MX ? Ws + (int64_t)n0 * kblk : Ws), (short)0, MX ? (int)((int64_t)rows_b * kblk) : 0,
         0x00020000);
     const int voS = (lw * 64 + lane) * kblk;
-    static_assert(kBN == 4 * 64 || !MX, "one 64-row slice of W scales per leading wave");
+    static_assert(kBN % 64 == 0, "whole 64-row slices of W scales");
     auto issue_scales = [&](uint32_t* dSA, uint32_t* dSB, int t) {
         if constexpr (MX) {
-            if (lw * 64 < kBM)      // short tiles: A has fewer rows than four slices
+            // A: slices starting past kBM rows (short tiles) are not loaded;
+            // the slice of a tile under 64 rows reads zeros past the tile's
+            // rows into the array's slack
+#pragma unroll
+            for (int sl = 0; sl * 4 * 64 < kBM; ++sl)
+                if ((lw + 4 * sl) * 64 < kBM)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                        rsSA, (__attribute__((address_space(3))) void*)(dSA + (lw + 4 * sl) * 64), 4,
+                        voS + 4 * sl * 64 * kblk + 4 * t, 0, 0, 0);
+#pragma unroll
+            for (int sl = 0; sl * 4 * 64 < kBN; ++sl)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    rsSA, (__attribute__((address_space(3))) void*)(dSA + lw * 64), 4, voS + 4 * t, 0, 0, 0);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rsSB, (__attribute__((address_space(3))) void*)(dSB + lw * 64), 4, voS + 4 * t, 0, 0, 0);
+                    rsSB, (__attribute__((address_space(3))) void*)(dSB + (lw + 4 * sl) * 64), 4,
+                    voS + 4 * sl * 64 * kblk + 4 * t, 0, 0, 0);
         }
     };
     // k0: byte offset of the K-step within a row (128 per step)
@@ -777,9 +826,12 @@ template <int MODE, bool MX>
 hipError_t launch_mode(const void* A, int64_t lda, const void* W, const uint8_t* As,
                        const uint8_t* Ws, int64_t M, int N, int K, const Epilogue& epi,
                        hipStream_t s) {
-    const int64_t tall = tile_count<MODE, 4>(M, N);
+    // The MXFP8 residual update with LayerNorm takes 64-row tiles: two
+    // 128 x 512 stages fill the LDS and leave no room for their scales.
+    constexpr int kTall = (MX && Shape<MODE, 4>::kWide) ? 2 : 4;
+    const int64_t tall = tile_count<MODE, kTall>(M, N);
     if (tall >= device_cus()) {
-        k_gemm_mfma<MODE, MX, 4><<<(unsigned)tall, kThreads, 0, s>>>(A, lda, W, As, Ws, M, N, K, epi);
+        k_gemm_mfma<MODE, MX, kTall><<<(unsigned)tall, kThreads, 0, s>>>(A, lda, W, As, Ws, M, N, K, epi);
     } else {
         const int64_t shorts = tile_count<MODE, 1>(M, N);
         k_gemm_mfma<MODE, MX, 1><<<(unsigned)shorts, kThreads, 0, s>>>(A, lda, W, As, Ws, M, N, K, epi);
@@ -836,6 +888,12 @@ hipError_t launch_gemm_mx(const uint8_t* A, const uint8_t* A_scales, const uint8
         case EPI_GELU_MX:
             if (N % 64 != 0 || epi.ldo % 64 != 0 || !epi.out_scales) return hipErrorInvalidValue;
             return launch_mode<EPI_GELU_MX, true>(A, K, W, A_scales, W_scales, M, N, K, epi, s);
+        case EPI_RESID_LN_MX:
+            // whole 64-column wave blocks (two scale bytes per row and wave)
+            if (epi.ldr % 4 != 0 || N > kResidLnMaxN || N % 64 != 0 || epi.ln_ldo % 64 != 0 ||
+                epi.ln_ldo < N || !epi.ln_gain || !epi.ln_shift || !epi.ln_out || !epi.ln_scales)
+                return hipErrorInvalidValue;
+            return launch_mode<EPI_RESID_LN_MX, true>(A, K, W, A_scales, W_scales, M, N, K, epi, s);
         default: return hipErrorInvalidValue;
     }
 }

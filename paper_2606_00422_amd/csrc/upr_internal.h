@@ -84,6 +84,9 @@ enum EpiMode : int {
     EPI_RESID_LN = 5,   // EPI_RESID, then ln_out[m, :] = LayerNorm(resid[m, :])
                         // (ln_gain, ln_shift, ln_eps; projection operand type);
                         // the tile spans whole rows, so N <= 512
+    EPI_RESID_LN_MX = 6,  // EPI_RESID_LN with the LayerNorm written as MXFP8:
+                          // codes -> ln_out (ln_ldo bytes per row), one E8M0
+                          // byte per 32 columns -> ln_scales (ln_ldo / 32 per row)
 };
 
 // Widest row (N) the residual update with LayerNorm (EPI_RESID_LN) handles.
@@ -114,6 +117,7 @@ struct Epilogue {
     float ln_eps;
     void* ln_out;
     int64_t ln_ldo;
+    void* ln_scales;        // EPI_RESID_LN_MX
 };
 
 // ---------------------------------------------------------------------------
@@ -145,7 +149,10 @@ hipError_t launch_mx_quantize(const T* x, int64_t rows, int k, uint8_t* codes, u
                               hipStream_t s);
 // MXFP8 projection GEMM: out = A W^T + epilogue with A [M, K] and W [N, K]
 // E4M3 codes and their E8M0 scales ([M, K/32], [N, K/32]); K a multiple of
-// 128; epilogue modes EPI_STORE, EPI_RESID and EPI_GELU_MX.
+// 128; epilogue modes EPI_STORE, EPI_RESID, EPI_GELU_MX and EPI_RESID_LN_MX.
+// EPI_RESID_LN_MX may write its LayerNorm into A itself (same rows, same
+// layout): a tile spans whole rows and writes them only after its last read
+// of A, and no other tile reads those rows.
 hipError_t launch_gemm_mx(const uint8_t* A, const uint8_t* A_scales, const uint8_t* W,
                           const uint8_t* W_scales, int64_t M, int N, int K, const Epilogue& epi,
                           hipStream_t s);

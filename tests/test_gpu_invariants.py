@@ -86,6 +86,26 @@ def test_tile_height_does_not_change_scores():
         assert np.array_equal(s[co[u]:co[u + 1]], batch[co[u]:co[u + 1]]), f"user {u}"
 
 
+def test_tile_height_does_not_change_scores_mxfp8():
+    """The same for the MXFP8 projection variant on the headline workload
+    (128,000 candidate rows: tall tiles in every projection, 64-row tiles for
+    the O projection with its fused LN2) against single-user calls (short
+    tiles, 64-candidate attention items)."""
+    inp = make_workload("u64_n1024_k2000", seed=5)
+    say(f"[gpu] mxfp8 tall vs short tiles: {int(inp.cand_offsets[-1])} candidate rows, then single users")
+    run = GpuRun(inp, model_dtype="bf16_mxfp8")
+    run.encode()
+    run.rank()
+    batch = run.scores_np().copy()
+    assert np.all(np.isfinite(batch))
+    ho, co = inp.hist_offsets, inp.cand_offsets
+    for u in [0, 37, inp.U - 1]:
+        run.scores.fill_(float("nan"))
+        run.rank(hoff=np.array([ho[u], ho[u + 1]], np.int32), coff=np.array([co[u], co[u + 1]], np.int32))
+        s = run.scores_np()
+        assert np.array_equal(s[co[u]:co[u + 1]], batch[co[u]:co[u + 1]]), f"user {u}"
+
+
 def test_sub_range_encode_matches_batch_encode():
     inp = _inp()
     say("[gpu] per-user encode")

@@ -539,19 +539,25 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
     constexpr int kTM = SH::kTM, kWM = SH::kWM;
     // Two LDS stages as separate arrays: the compiler can then tell that
     // fragment reads of one stage do not alias the loads filling the other.
+    // Short 256-wide tiles (small calls: one tile per compute unit, the
+    // K-loop waits on each stage's round trip) keep a third stage and load
+    // two K-steps ahead.
+    constexpr int kStages = (!SH::kWide && TM == 1) ? 3 : 2;
     __shared__ __attribute__((aligned(16))) f16 sA0[kBM * kBK];
     __shared__ __attribute__((aligned(16))) f16 sA1[kBM * kBK];
+    __shared__ __attribute__((aligned(16))) f16 sA2[kStages == 3 ? kBM * kBK : 8];
     __shared__ __attribute__((aligned(16))) f16 sB0[kBN * kBK];
     __shared__ __attribute__((aligned(16))) f16 sB1[kBN * kBK];
+    __shared__ __attribute__((aligned(16))) f16 sB2[kStages == 3 ? kBN * kBK : 8];
     // MXFP8: the K-step's scale dword of every row of A and of W
     // (at least one 64-row slice each: a slice is one load instruction)
     constexpr int kSA = MX ? (kBM < 64 ? 64 : kBM) : 1, kSB = MX ? kBN : 1;
     __shared__ uint32_t sSA0[kSA], sSA1[kSA], sSB0[kSB], sSB1[kSB];
+    __shared__ uint32_t sSA2[kStages == 3 ? kSA : 1], sSB2[kStages == 3 ? kSB : 1];
     // Epilogue staging of short 256-wide tiles (their A stages are too small
-    // to hold it): one region per wave
+    // to hold it): one region per wave, three in each of the W stages
     constexpr int kShortRegion = 32 * kStage32 * 4;
-    constexpr bool kOwnStaging = !SH::kWide && TM < 4;
-    __shared__ __attribute__((aligned(16))) char sR[kOwnStaging ? kThreads / 64 * kShortRegion : 16];
+    static_assert(kStages == 2 || SH::kWide || 3 * kShortRegion <= kBN * kBK * 2, "staging fits a stage");
     constexpr int kEB = MX ? 1 : 2;         // bytes per operand value
     const char* const A = static_cast<const char*>(Av);
     const char* const W = static_cast<const char*>(Wv);
@@ -754,19 +760,68 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
         __builtin_amdgcn_sched_barrier(0);
     };
 
-    if (lead) {
-        issue_loads(sA0, sB0, 0);
-        issue_scales(sSA0, sSB0, 0);
+    if constexpr (kStages == 3) {
+        // Step t reads stage t % 3 and its leading waves fill stage
+        // (t + 2) % 3, last read in step t - 1 (by the trailing waves before
+        // the barrier that ended it); at its end only step t + 1's loads must
+        // have landed, so step t + 2's stay in flight.  Leading wave 0 may
+        // hold one more load (A's scales) than the count and then waits for
+        // it too.
+        auto kstep3 = [&](const f16* cA, const f16* cB, const uint32_t* cSA, const uint32_t* cSB,
+                          f16* nA, f16* nB, uint32_t* nSA, uint32_t* nSB, int t) {
+            if (lead && t + 2 < nk) {
+                issue_loads(nA, nB, (t + 2) * kBK * 2);
+                issue_scales(nSA, nSB, t + 2);
+            }
+            read_frags(cA, cB, cSA, cSB);
+            __builtin_amdgcn_s_waitcnt(0xC07F);     // lgkmcnt(0): fragments in registers
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+            compute();
+            __builtin_amdgcn_sched_barrier(0);
+            constexpr int kInFlight = kLoadsA + kLoadsB + (MX ? 1 : 0);
+            static_assert(kInFlight < 16, "vmcnt field");
+            if (t + 2 < nk)
+                __builtin_amdgcn_s_waitcnt(0x0F70 | kInFlight);   // vmcnt(step t+2's loads)
+            else
+                __builtin_amdgcn_s_waitcnt(0x0F70);               // vmcnt(0)
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        if (lead) {
+            issue_loads(sA0, sB0, 0);
+            issue_scales(sSA0, sSB0, 0);
+            if (nk > 1) {
+                issue_loads(sA1, sB1, kBK * 2);
+                issue_scales(sSA1, sSB1, 1);
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (!lead) __builtin_amdgcn_s_barrier();
+        int kt = 0;
+        for (; kt + 3 <= nk; kt += 3) {
+            kstep3(sA0, sB0, sSA0, sSB0, sA2, sB2, sSA2, sSB2, kt);
+            kstep3(sA1, sB1, sSA1, sSB1, sA0, sB0, sSA0, sSB0, kt + 1);
+            kstep3(sA2, sB2, sSA2, sSB2, sA1, sB1, sSA1, sSB1, kt + 2);
+        }
+        if (kt < nk) kstep3(sA0, sB0, sSA0, sSB0, sA2, sB2, sSA2, sSB2, kt);
+        if (kt + 1 < nk) kstep3(sA1, sB1, sSA1, sSB1, sA0, sB0, sSA0, sSB0, kt + 1);
+    } else {
+        if (lead) {
+            issue_loads(sA0, sB0, 0);
+            issue_scales(sSA0, sSB0, 0);
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (!lead) __builtin_amdgcn_s_barrier();
+        int kt = 0;
+        for (; kt + 2 <= nk; kt += 2) {
+            kstep(sA0, sB0, sSA0, sSB0, sA1, sB1, sSA1, sSB1, kt);
+            kstep(sA1, sB1, sSA1, sSB1, sA0, sB0, sSA0, sSB0, kt + 1);
+        }
+        if (kt < nk) kstep(sA0, sB0, sSA0, sSB0, sA1, sB1, sSA1, sSB1, kt);
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (!lead) __builtin_amdgcn_s_barrier();
-    int kt = 0;
-    for (; kt + 2 <= nk; kt += 2) {
-        kstep(sA0, sB0, sSA0, sSB0, sA1, sB1, sSA1, sSB1, kt);
-        kstep(sA1, sB1, sSA1, sSB1, sA0, sB0, sSA0, sSB0, kt + 1);
-    }
-    if (kt < nk) kstep(sA0, sB0, sSA0, sSB0, sA1, sB1, sSA1, sSB1, kt);
     // Past here every wave has finished its fragment reads (the trailing
     // waves' last reads precede the barrier that ended the leading waves'
     // last step), so the stages are free for the epilogue.
@@ -789,8 +844,11 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
     } else {
         const int wsel = __builtin_amdgcn_readfirstlane(wave) >> 1;
         f16* const sbase = wsel == 0 ? sA0 : wsel == 1 ? sA1 : wsel == 2 ? sB0 : sB1;
-        char* const region = kOwnStaging ? sR + wave * kShortRegion
-                                         : reinterpret_cast<char*>(sbase) + (wave & 1) * kRegionBytes;
+        const int w3 = __builtin_amdgcn_readfirstlane(wave) / 3;
+        char* const region =
+            kStages == 3 ? reinterpret_cast<char*>(w3 == 0 ? sB0 : w3 == 1 ? sB1 : sB2) +
+                               (__builtin_amdgcn_readfirstlane(wave) % 3) * kShortRegion
+                         : reinterpret_cast<char*>(sbase) + (wave & 1) * kRegionBytes;
         // Epilogues writing new outputs start only after the trailing
         // waves' last MFMAs (overlapping them measured 4-5% slower); the
         // residual update, which reads as much as it writes, overlaps them.

@@ -10,12 +10,14 @@
 //
 // Main loop.  A and W tiles go straight from global memory into LDS
 // (buffer loads with the LDS bit: no staging registers; rows past the end
-// read as zeros), in two stages.  LDS rows are 128 bytes (64 fp16) whose
-// eight 16-byte chunks are XOR-swizzled, so fragment reads are bank-conflict
-// free.  The two waves sharing a SIMD (w and w+4) run in opposite phases
-// ("ping-pong"): while one reads its operand fragments from LDS into
-// registers, the other runs its MFMAs, and they swap at each barrier.  Only
-// the four leading waves issue the global loads, one K-step ahead.
+// read as zeros), in two stages (three for the short tiles of small calls,
+// whose K-loop waits on the load round trip).  LDS rows are 128 bytes (64
+// fp16) whose eight 16-byte chunks are XOR-swizzled, so fragment reads are
+// bank-conflict free.  The two waves sharing a SIMD (w and w+4) run in
+// opposite phases ("ping-pong"): while one reads its operand fragments from
+// LDS into registers, the other runs its MFMAs, and they swap at each
+// barrier.  Only the four leading waves issue the global loads, one K-step
+// ahead (two with three stages).
 //
 // Epilogue.  Stores straight from the MFMA layout touch 32 rows per
 // instruction with 8-16 bytes each and reach about 60% of the bandwidth of

@@ -58,6 +58,9 @@ SMALL = [
     ([0, 1, 63, 65, 130, 300], [1, 129, 0, 257, 64, 3], 128, 2, 2, 256, "bf16"),
     ([200, 0, 17], [300, 40, 1], 64, 2, 2, 128, "f32"),
     ([511, 5, 1000], [7, 513, 250], 256, 4, 1, 512, "bf16"),
+    # rows that fill no tile width: q|k|v 1152 and FFN 768 columns, and the
+    # fused LayerNorm tile with two of its eight column blocks empty
+    ([100, 7, 600], [300, 65, 20], 384, 6, 2, 768, "bf16"),
     # rows wider than the fused residual+LayerNorm tile (512): separate
     # LayerNorm launches
     ([40, 300], [70, 129], 1024, 16, 2, 1024, "bf16"),

@@ -189,7 +189,26 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
         const unsigned ldr4 = (unsigned)epi.ldr * 4u;
         const unsigned vo = col_ok ? (unsigned)rsub * ldr4 + (unsigned)col * 4u : 0x80000000u;
         float4 g[2][8];                     // residual rows of passes i (even/odd)
+        // bf16 residual source (first layer: the tokens), same rows and
+        // columns at half the byte offsets; a lane past N keeps an offset
+        // (2^30) beyond the range
+        const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<unsigned short*>(static_cast<const unsigned short*>(epi.resid_src)) + wrow0 * epi.ldr,
+            (short)0, (int)(rows_valid * epi.ldr * 2), 0x00020000);
+        const bool from_src = epi.resid_src != nullptr;
         auto load_resid = [&](int i, float4 (&dst)[8]) {
+            if (from_src) {
+                typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
+#pragma unroll
+                for (int p = 0; p < 8; ++p) {
+                    const u32x2 w = __builtin_bit_cast(
+                        u32x2, __builtin_amdgcn_raw_buffer_load_b64(
+                                   rsrc, (vo + (unsigned)(i * 32 + p * 4) * ldr4) >> 1, 0, 0));
+                    dst[p] = make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
+                                         __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u));
+                }
+                return;
+            }
 #pragma unroll
             for (int p = 0; p < 8; ++p)
                 dst[p] = __builtin_bit_cast(

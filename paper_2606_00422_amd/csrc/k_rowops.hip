@@ -137,7 +137,8 @@ __device__ __forceinline__ void store_normed_mx(uint8_t* __restrict__ codes,
 }
 
 // g = float(x); a = LN(g)  (residual stream initialisation fused with the
-// first layer's LayerNorm).
+// first layer's LayerNorm).  g may be null: the first residual update then
+// reads x itself.
 template <bool VEC, typename TKV, typename TA>
 __global__ __launch_bounds__(256) void k_init_layernorm(const TKV* __restrict__ x,
                                                         float* __restrict__ g, TA* __restrict__ a,
@@ -160,7 +161,8 @@ __global__ __launch_bounds__(256) void k_init_layernorm(const TKV* __restrict__ 
         for (int i = 0; i < kMaxPerLane; ++i)
             if (i < per) v[i] = to_f(xr[lane + 64 * i]);
     }
-    if (VEC) {
+    if (g == nullptr) {
+    } else if (VEC) {
 #pragma unroll
         for (int j = 0; j < kMaxPerLane / 4; ++j)
             if (4 * j < per)
@@ -212,8 +214,9 @@ __global__ __launch_bounds__(256) void k_layernorm_mx(const TKV* __restrict__ x,
             if (4 * j < per) {
                 const int c = j * 256 + 4 * lane;
                 load4(xr + c, v + 4 * j);
-                *reinterpret_cast<float4*>(gr + c) =
-                    make_float4(v[4 * j], v[4 * j + 1], v[4 * j + 2], v[4 * j + 3]);
+                if (g != nullptr)      // null: the first residual update reads x
+                    *reinterpret_cast<float4*>(gr + c) =
+                        make_float4(v[4 * j], v[4 * j + 1], v[4 * j + 2], v[4 * j + 3]);
             }
     } else {
         load_row<true>(g + row * d, d, lane, v);

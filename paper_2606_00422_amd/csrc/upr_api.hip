@@ -285,8 +285,9 @@ static upr_status rank_layers_mx(const upr_model* m, const upr_kv_cache* cache,
     uint8_t* hc = reinterpret_cast<uint8_t*>(ws + p.off_h);
     uint8_t* hsc = hc + align256((size_t)R * F);
     const float qscale = 1.4426950408889634f / std::sqrt((float)D);
+    // the first O projection reads the residual from the tokens
     UPR_LAUNCH("rank.init_ln1",
-               launch_init_layernorm_mx<bf16>(cand_emb + p.row0 * d, g, ac, asc, R, d,
+               launch_init_layernorm_mx<bf16>(cand_emb + p.row0 * d, nullptr, ac, asc, R, d,
                                               m->layers[0].ln1_g, m->layers[0].ln1_b, c.ln_eps, s));
     if (p.use_mfma_attn)
         UPR_LAUNCH("rank.worklist",
@@ -344,7 +345,8 @@ static upr_status rank_layers_mx(const upr_model* m, const upr_kv_cache* cache,
                                                           cache->capacity_rows, s));
             UPR_LAUNCH("rank.quant_o", launch_mx_quantize<f16>(o, R, d, ac, asc, s));
         }
-        const Epilogue r = resid_epilogue(w.bo, fuse ? w.ln2_g : nullptr, w.ln2_b);
+        Epilogue r = resid_epilogue(w.bo, fuse ? w.ln2_g : nullptr, w.ln2_b);
+        if (l == 0) r.resid_src = cand_emb + p.row0 * d;
         UPR_LAUNCH("rank.gemm_o", launch_gemm_mx(ac, asc, w.mx_o, w.mx_o_s, R, d, d, r, s));
         if (!fuse)
             UPR_LAUNCH("rank.ln2", launch_layernorm_mx(g, ac, asc, R, d, w.ln2_g, w.ln2_b, c.ln_eps, s));
@@ -372,13 +374,15 @@ static bool fused_layernorm(const upr_config& c) {
 // Attention-output projection and FFN of one layer, on the fp32 residual g:
 // g += o Wo^T + bo;  a = LN2(g);  h = gelu(a W1^T + b1);  g += h W2^T + b2;
 // then, when next_g is given and the LayerNorm is fused, a = LN(g) with
-// (next_g, next_b).  Timing scopes are named "<stage>.gemm_o" etc.
+// (next_g, next_b).  resid_src (first layer, bf16 models): g is not yet
+// written and the O projection reads the residual from these token rows.
+// Timing scopes are named "<stage>.gemm_o" etc.
 template <typename Types>
 static hipError_t launch_ffn_block(const char* const names[4], const upr_config& c,
                                    const LayerWeights& w, const typename Types::act* o,
                                    typename Types::act* a, typename Types::act* h, float* g,
                                    int64_t R, const float* next_g, const float* next_b,
-                                   hipStream_t s) {
+                                   const void* resid_src, hipStream_t s) {
     using T = typename Types::kv;
     using TA = typename Types::act;
     const int d = c.d_model, F = c.d_ff;
@@ -396,6 +400,7 @@ static hipError_t launch_ffn_block(const char* const names[4], const upr_config&
     r.ln_eps = eps;
     r.ln_out = a;
     r.ln_ldo = d;
+    r.resid_src = resid_src;
     {
         ProfScope ps(names[0], s);
         e = launch_gemm<TA, T>(o, d, static_cast<const TA*>(w.Wo), R, d, d, r, s);
@@ -418,6 +423,7 @@ static hipError_t launch_ffn_block(const char* const names[4], const upr_config&
     }
     if (e != hipSuccess) return e;
     r.mode = fuse && next_g ? EPI_RESID_LN : EPI_RESID;
+    r.resid_src = nullptr;
     r.acc_scale = w.s_2;
     r.bias = w.b2;
     r.ln_gain = next_g;
@@ -446,9 +452,11 @@ static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_
     TA* o = reinterpret_cast<TA*>(ws + p.off_o);
     TA* h = reinterpret_cast<TA*>(ws + p.off_h);
     const float qscale = 1.4426950408889634f / std::sqrt((float)D);
+    // bf16 models: the first O projection reads the residual from the tokens
+    const bool tok_resid = std::is_same_v<Types, Bf16Types>;
     UPR_LAUNCH("encode.init_ln1",
-               launch_init_layernorm<T, TA>(hist_emb + p.row0 * d, g, a, R, d, m->layers[0].ln1_g,
-                                            m->layers[0].ln1_b, c.ln_eps, s));
+               launch_init_layernorm<T, TA>(hist_emb + p.row0 * d, tok_resid ? nullptr : g, a, R, d,
+                                            m->layers[0].ln1_g, m->layers[0].ln1_b, c.ln_eps, s));
     if (p.use_mfma_attn && c.n_layers > 1)
         UPR_LAUNCH("encode.worklist",
                    launch_attn_worklist(hist->offsets_dev, hist->offsets_dev, hist->num_users, H,
@@ -497,7 +505,8 @@ static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_
                                                         static_cast<const T*>(e.cache_v),
                                                         cache->capacity_rows, s));
         const LayerWeights& wn = m->layers[l + 1];     // l + 1 < n_layers here
-        UPR_HIP(launch_ffn_block<Types>(kEncodeFfnNames, c, w, o, a, h, g, R, wn.ln1_g, wn.ln1_b, s));
+        UPR_HIP(launch_ffn_block<Types>(kEncodeFfnNames, c, w, o, a, h, g, R, wn.ln1_g, wn.ln1_b,
+                                        tok_resid && l == 0 ? hist_emb + p.row0 * d : nullptr, s));
     }
     return UPR_OK;
 }
@@ -537,9 +546,11 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
         }
     }
     if (!mx_done) {
+    // bf16 models: the first O projection reads the residual from the tokens
+    const bool tok_resid = std::is_same_v<Types, Bf16Types>;
     UPR_LAUNCH("rank.init_ln1",
-               launch_init_layernorm<T, TA>(cand_emb + p.row0 * d, g, a, R, d, m->layers[0].ln1_g,
-                                            m->layers[0].ln1_b, c.ln_eps, s));
+               launch_init_layernorm<T, TA>(cand_emb + p.row0 * d, tok_resid ? nullptr : g, a, R, d,
+                                            m->layers[0].ln1_g, m->layers[0].ln1_b, c.ln_eps, s));
     if (p.use_mfma_attn)
         UPR_LAUNCH("rank.worklist", launch_attn_worklist(cand->offsets_dev, hist->offsets_dev, cand->num_users, H,
                                      p.attn_tile, false, reinterpret_cast<int32_t*>(ws + p.off_work),
@@ -578,7 +589,8 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
         const bool last = l + 1 == c.n_layers;
         const float* ng = !last ? m->layers[l + 1].ln1_g : out.heads ? m->fin.lnf_g : nullptr;
         const float* nb = !last ? m->layers[l + 1].ln1_b : out.heads ? m->fin.lnf_b : nullptr;
-        UPR_HIP(launch_ffn_block<Types>(kRankFfnNames, c, w, o, a, h, g, R, ng, nb, s));
+        UPR_HIP(launch_ffn_block<Types>(kRankFfnNames, c, w, o, a, h, g, R, ng, nb,
+                                        tok_resid && l == 0 ? cand_emb + p.row0 * d : nullptr, s));
     }
     }  // !mx_done
     if (!out.heads) {

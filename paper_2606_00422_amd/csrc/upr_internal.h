@@ -118,6 +118,10 @@ struct Epilogue {
     void* ln_out;
     int64_t ln_ldo;
     void* ln_scales;        // EPI_RESID_LN_MX
+    // EPI_RESID*: when set, the residual is read from these bf16 rows
+    // (leading dimension ldr) instead of resid, and the sum still goes to
+    // resid: the first layer's update reads the tokens themselves
+    const void* resid_src;
 };
 
 // ---------------------------------------------------------------------------

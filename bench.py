@@ -57,8 +57,9 @@ def kernel_work(inp):
         "rank.ln1": ("hbm", R * d * (4.0 + es)),
         "rank.ln2": ("hbm", R * d * (4.0 + es)),
         "rank.score_head": ("hbm", R * d * 4.0 + R * 4.0),
-        # read the tokens, write the fp32 residual and the normalised row
-        "rank.init_ln1": ("hbm", R * d * (es + 4.0 + es)),
+        # read the tokens, write the normalised row (and, for fp32 models,
+        # the fp32 residual: bf16 models' first O projection reads the tokens)
+        "rank.init_ln1": ("hbm", R * d * (es + es) if inp.dtype == "bf16" else R * d * (es + 4.0 + es)),
     }
 
 

@@ -85,7 +85,7 @@ constexpr int kCPR = kBK / 8;                      // 16-byte chunks per LDS row
 // four leading waves).
 template <int MODE, int TM>
 struct Shape {
-    static constexpr bool kWide = MODE == EPI_RESID_LN || MODE == EPI_RESID_LN_MX;
+    static constexpr bool kWide = MODE == EPI_RESID_LN || MODE == EPI_RESID_LN_MX || MODE == EPI_RESID_SCORE;
     static constexpr int kTM = TM, kWM = 32 * TM;
     static constexpr int kBM = kWide ? kWM : 2 * kWM, kBN = kWide ? 512 : 256;
     static constexpr int kWavesN = kWide ? 8 : 4;
@@ -166,12 +166,15 @@ __device__ __forceinline__ unsigned pack2(float a, float b) {
 template <int MODE, int kTM>
 __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* const region,
                                            int64_t wrow0, int wcol0, int64_t M, int N,
-                                           const Epilogue& epi, int lane, float* const lnx, int wn) {
+                                           const Epilogue& epi, int lane, float* const lnx, int wn,
+                                           float* const scx = nullptr) {
     constexpr int kWM = 32 * kTM;           // rows of the wave tile
     const int lrow = lane & 31, lhalf = lane >> 5;
     const float sc = epi.acc_scale;
-    if constexpr (MODE == EPI_RESID || MODE == EPI_RESID_LN || MODE == EPI_RESID_LN_MX) {
+    if constexpr (MODE == EPI_RESID || MODE == EPI_RESID_LN || MODE == EPI_RESID_LN_MX ||
+                  MODE == EPI_RESID_SCORE) {
         constexpr bool kLN = MODE != EPI_RESID, kLnMx = MODE == EPI_RESID_LN_MX;
+        constexpr bool kScore = MODE == EPI_RESID_SCORE;
         const int ch = lane & 15, rsub = lane >> 4;
         const int col = wcol0 + ch * 4;
         const bool col_ok = col < N;                  // N is a multiple of 8
@@ -217,15 +220,19 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
         float4 ln_g = make_float4(0.f, 0.f, 0.f, 0.f), ln_b = ln_g;
         __amdgpu_buffer_rsrc_t rln = rs, rlns = rs;
         unsigned lnld2 = 0, vln = 0x80000000u, lnsld = 0, vlns = 0x80000000u;
+        float4 sw = make_float4(0.f, 0.f, 0.f, 0.f);    // EPI_RESID_SCORE: score weights
         if constexpr (kLN) {
+            if (col_ok) {
+                ln_g = *reinterpret_cast<const float4*>(epi.ln_gain + col);
+                ln_b = *reinterpret_cast<const float4*>(epi.ln_shift + col);
+                if constexpr (kScore) sw = *reinterpret_cast<const float4*>(epi.score_w + col);
+            }
+        }
+        if constexpr (kLN && !kScore) {
             // LN output rows through a descriptor ending at row M, like the
             // residual; 16-bit values, or MXFP8 codes (and a second
             // descriptor over the scale bytes), four per lane.
             constexpr int kOB = kLnMx ? 1 : 2;      // bytes per output value
-            if (col_ok) {
-                ln_g = *reinterpret_cast<const float4*>(epi.ln_gain + col);
-                ln_b = *reinterpret_cast<const float4*>(epi.ln_shift + col);
-            }
             rln = __builtin_amdgcn_make_buffer_rsrc(static_cast<char*>(epi.ln_out) + wrow0 * epi.ln_ldo * kOB,
                                                     (short)0, (int)(rows_valid * epi.ln_ldo * kOB), 0x00020000);
             lnld2 = (unsigned)epi.ln_ldo * kOB;
@@ -311,6 +318,43 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
                 M2 += fmaf(n_w[w] * dm, dm, m2_w[w]);
             }
             const float rstd = 1.0f / sqrtf(M2 / tot + epi.ln_eps);
+            if constexpr (kScore) {
+                // per row, this wave's share of LN(row) . w over its four
+                // columns per lane, summed over the row group like the
+                // statistics; the waves' shares meet in scx at a second
+                // workgroup barrier, and lane l < 32 adds the eight of row
+                // l in wave order
+                float t2[8];
+#pragma unroll
+                for (int p = 0; p < 8; ++p) {
+                    const float mu_p = __shfl(mu, p * 4 + rsub, 64);
+                    const float rs_p = __shfl(rstd, p * 4 + rsub, 64);
+                    const float4 h = hv[p];
+                    float d4 = 0.f;
+                    if (col_ok) {
+                        d4 = fmaf(fmaf((h.x - mu_p) * rs_p, ln_g.x, ln_b.x), sw.x, d4);
+                        d4 = fmaf(fmaf((h.y - mu_p) * rs_p, ln_g.y, ln_b.y), sw.y, d4);
+                        d4 = fmaf(fmaf((h.z - mu_p) * rs_p, ln_g.z, ln_b.z), sw.z, d4);
+                        d4 = fmaf(fmaf((h.w - mu_p) * rs_p, ln_g.w, ln_b.w), sw.w, d4);
+                    }
+                    t2[p] = d4;
+                }
+                const float prow = rows8_sum(t2);
+                float* const S = scx + (i & 1) * (32 * 8);
+                if ((ch & 1) == 0) S[((ch >> 1) * 4 + rsub) * 8 + wn] = prow;
+                __builtin_amdgcn_s_waitcnt(0xC07F);
+                asm volatile("" ::: "memory");
+                __builtin_amdgcn_s_barrier();
+                asm volatile("" ::: "memory");
+                const int64_t row = wrow0 + i * 32 + lrow;
+                if (wn == 0 && lhalf == 0 && row < M) {
+                    const float4 a0 = *reinterpret_cast<const float4*>(S + lrow * 8);
+                    const float4 a1 = *reinterpret_cast<const float4*>(S + lrow * 8 + 4);
+                    const float sc = ((((((a0.x + a0.y) + a0.z) + a0.w) + a1.x) + a1.y) + a1.z) + a1.w;
+                    epi.score_out[row] = sc + *epi.score_b;
+                }
+                return;
+            }
             // LN of this lane's four columns of rows p*4 + rsub
 #pragma unroll
             for (int p = 0; p < 8; ++p) {
@@ -374,8 +418,9 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
                 const u32x4 o = __builtin_bit_cast(
                     u32x4, make_float4(r.x + fmaf(x[p].x, sc, bias4.x), r.y + fmaf(x[p].y, sc, bias4.y),
                                        r.z + fmaf(x[p].z, sc, bias4.z), r.w + fmaf(x[p].w, sc, bias4.w)));
-                __builtin_amdgcn_raw_buffer_store_b128(o, rs, vo + (unsigned)(i * 32 + p * 4) * ldr4, 0,
-                                                       2 /* nt */);
+                if constexpr (!kScore)
+                    __builtin_amdgcn_raw_buffer_store_b128(o, rs, vo + (unsigned)(i * 32 + p * 4) * ldr4, 0,
+                                                           2 /* nt */);
                 if constexpr (kLN) hv[p] = __builtin_bit_cast(float4, o);
             }
             if constexpr (kLN) ln_pass(i);
@@ -860,8 +905,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
         constexpr int kRegion = 32 * kStage32 * 4;
         char* const region = wave < 7 ? reinterpret_cast<char*>(sB0) + wave * kRegion
                                       : reinterpret_cast<char*>(sB1);
+        // (EPI_RESID_SCORE: the waves' score shares go to sA1)
         store_tile<MODE, kTM>(acc, region, m0 + wm * kWM, n0 + wn * kWN, M, N, epi, lane,
-                              reinterpret_cast<float*>(sA0), wn);
+                              reinterpret_cast<float*>(sA0), wn, reinterpret_cast<float*>(sA1));
     } else {
         const int wsel = __builtin_amdgcn_readfirstlane(wave) >> 1;
         f16* const sbase = wsel == 0 ? sA0 : wsel == 1 ? sA1 : wsel == 2 ? sB0 : sB1;
@@ -942,6 +988,11 @@ hipError_t launch_gemm_mfma(const f16* A, int64_t lda, const f16* W, int64_t M, 
                 !epi.ln_gain || !epi.ln_shift || !epi.ln_out)
                 return hipErrorInvalidValue;
             return launch_mode<EPI_RESID_LN, false>(A, lda, W, nullptr, nullptr, M, N, K, epi, s);
+        case EPI_RESID_SCORE:
+            if (epi.ldr % 4 != 0 || N > kResidLnMaxN || !epi.ln_gain || !epi.ln_shift ||
+                !epi.score_w || !epi.score_b || !epi.score_out)
+                return hipErrorInvalidValue;
+            return launch_mode<EPI_RESID_SCORE, false>(A, lda, W, nullptr, nullptr, M, N, K, epi, s);
         case EPI_QKV_CACHE:
             if (epi.ldo % 8 != 0 || epi.head_dim % 8 != 0 || epi.d_model % 8 != 0)
                 return hipErrorInvalidValue;

@@ -376,13 +376,16 @@ static bool fused_layernorm(const upr_config& c) {
 // then, when next_g is given and the LayerNorm is fused, a = LN(g) with
 // (next_g, next_b).  resid_src (first layer, bf16 models): g is not yet
 // written and the O projection reads the residual from these token rows.
+// scores (last ranking layer, fused LayerNorms): FFN down ends in the score
+// head, scores[m] = LN_f(g[m]) . w + b with score_fin, and g is left stale.
 // Timing scopes are named "<stage>.gemm_o" etc.
 template <typename Types>
 static hipError_t launch_ffn_block(const char* const names[4], const upr_config& c,
                                    const LayerWeights& w, const typename Types::act* o,
                                    typename Types::act* a, typename Types::act* h, float* g,
                                    int64_t R, const float* next_g, const float* next_b,
-                                   const void* resid_src, hipStream_t s) {
+                                   const void* resid_src, const FinalWeights* score_fin,
+                                   float* scores, hipStream_t s) {
     using T = typename Types::kv;
     using TA = typename Types::act;
     const int d = c.d_model, F = c.d_ff;
@@ -424,6 +427,14 @@ static hipError_t launch_ffn_block(const char* const names[4], const upr_config&
     if (e != hipSuccess) return e;
     r.mode = fuse && next_g ? EPI_RESID_LN : EPI_RESID;
     r.resid_src = nullptr;
+    if (fuse && scores != nullptr) {
+        r.mode = EPI_RESID_SCORE;
+        next_g = score_fin->lnf_g;
+        next_b = score_fin->lnf_b;
+        r.score_w = score_fin->w_score;
+        r.score_b = score_fin->b_score;
+        r.score_out = scores;
+    }
     r.acc_scale = w.s_2;
     r.bias = w.b2;
     r.ln_gain = next_g;
@@ -506,7 +517,8 @@ static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_
                                                         cache->capacity_rows, s));
         const LayerWeights& wn = m->layers[l + 1];     // l + 1 < n_layers here
         UPR_HIP(launch_ffn_block<Types>(kEncodeFfnNames, c, w, o, a, h, g, R, wn.ln1_g, wn.ln1_b,
-                                        tok_resid && l == 0 ? hist_emb + p.row0 * d : nullptr, s));
+                                        tok_resid && l == 0 ? hist_emb + p.row0 * d : nullptr,
+                                        nullptr, nullptr, s));
     }
     return UPR_OK;
 }
@@ -589,13 +601,18 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
         const bool last = l + 1 == c.n_layers;
         const float* ng = !last ? m->layers[l + 1].ln1_g : out.heads ? m->fin.lnf_g : nullptr;
         const float* nb = !last ? m->layers[l + 1].ln1_b : out.heads ? m->fin.lnf_b : nullptr;
+        // the score head rides on the last FFN down when the LayerNorms are fused
+        float* const fused_scores =
+            l + 1 == c.n_layers && !out.heads && fused_layernorm<Types>(c) ? out.scores + p.row0 : nullptr;
         UPR_HIP(launch_ffn_block<Types>(kRankFfnNames, c, w, o, a, h, g, R, ng, nb,
-                                        tok_resid && l == 0 ? cand_emb + p.row0 * d : nullptr, s));
+                                        tok_resid && l == 0 ? cand_emb + p.row0 * d : nullptr,
+                                        &m->fin, fused_scores, s));
     }
     }  // !mx_done
     if (!out.heads) {
-        UPR_LAUNCH("rank.score_head",
-                   launch_score_head(g, out.scores + p.row0, R, d, m->fin, c.ln_eps, s));
+        if (mx_done || !fused_layernorm<Types>(c))
+            UPR_LAUNCH("rank.score_head",
+                       launch_score_head(g, out.scores + p.row0, R, d, m->fin, c.ln_eps, s));
         return UPR_OK;
     }
     // action heads: z = LN_f(g); hid = gelu(z W1^T + b1) (all heads stacked);

@@ -87,6 +87,10 @@ enum EpiMode : int {
     EPI_RESID_LN_MX = 6,  // EPI_RESID_LN with the LayerNorm written as MXFP8:
                           // codes -> ln_out (ln_ldo bytes per row), one E8M0
                           // byte per 32 columns -> ln_scales (ln_ldo / 32 per row)
+    EPI_RESID_SCORE = 7,  // the last residual update, then the score head:
+                          // score_out[m] = LN(resid[m, :]) . score_w + *score_b
+                          // (ln_gain, ln_shift, ln_eps = LN_f); the updated
+                          // residual itself is not stored; N <= 512
 };
 
 // Widest row (N) the residual update with LayerNorm (EPI_RESID_LN) handles.
@@ -122,6 +126,10 @@ struct Epilogue {
     // (leading dimension ldr) instead of resid, and the sum still goes to
     // resid: the first layer's update reads the tokens themselves
     const void* resid_src;
+    // EPI_RESID_SCORE
+    const float* score_w;   // [N]
+    const float* score_b;   // one value
+    float* score_out;       // [M]
 };
 
 // ---------------------------------------------------------------------------

@@ -44,8 +44,9 @@ def kernel_work(inp):
     k = inp.cand_lens
     es = 2 if inp.dtype == "bf16" else 4
     attn_pairs = int(np.sum(k * (n + 1)))
-    # (gemm_o and gemm_down also apply the LayerNorm that follows them when a
-    # row fits their tile: d <= 512; their figure stays the projection FLOPs)
+    # (gemm_o and gemm_down also apply the LayerNorm that follows them, and
+    # the last gemm_down the score head, when a row fits their tile: d <= 512;
+    # their figure stays the projection FLOPs)
     return {
         "rank.gemm_qkv": ("mfma", 2.0 * R * 3 * d * d),
         "rank.gemm_o": ("mfma", 2.0 * R * d * d),

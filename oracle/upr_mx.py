@@ -104,12 +104,6 @@ def mx_round(x):
     return mx_dequantize(*mx_quantize(x))
 
 
-def f16_round(x):
-    """x rounded to IEEE half precision as a GPU rounds an fp32 value: to
-    fp32 first, then to the nearest fp16, ties to even (numpy's casts)."""
-    return np.asarray(x, dtype=np.float32).astype(np.float16).astype(np.float64)
-
-
 def linear_mx(x, W, b):
     """x W^T + b with x (rows) and W (rows of the [out, in] matrix) both
     MXFP8-encoded along the input axis; the products and sums are exact

@@ -220,16 +220,18 @@ def encode(blob, d, H, L, F, hist_emb, hist_offsets, capacity_rows=None, users=N
 
 
 def _projection_rule(proj):
-    """(linear map, what the O projection's input goes through first) for the
-    exact model or the MXFP8 projection variant (oracle/upr_mx.py): every
-    projection input and weight MXFP8-encoded along the contraction axis, the
-    attention output first held in fp16 (the precision it is materialised
-    in before it is encoded)."""
+    """Linear map of the four projections of a ranking layer: the exact
+    model's, or the MXFP8 projection variant's (oracle/upr_mx.py).  The paper
+    runs the forward pass in FP8 with E4M3, quantizing the inputs of its fused
+    LayerNorm/linear/activation modules (Sec. 3, "FP8 quantization"): here
+    every projection input (LN1 output, attention output, LN2 output, GELU
+    output) and every projection weight is MXFP8-encoded from its exact value
+    along the contraction axis, and nothing else is rounded."""
     if proj == "exact":
-        return linear, (lambda o: o)
+        return linear
     if proj == "mxfp8":
-        from .upr_mx import f16_round, linear_mx
-        return linear_mx, f16_round
+        from .upr_mx import linear_mx
+        return linear_mx
     raise ValueError(f"unknown projection rule {proj!r}")
 
 
@@ -250,7 +252,7 @@ def rank_hidden(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
     independent, so a subset is exact.  ``proj="mxfp8"`` runs the four
     projections of every layer in MXFP8 (see ``_projection_rule``).
     """
-    lin, o_in = _projection_rule(proj)
+    lin = _projection_rule(proj)
     layers, final = unpack_weights(blob, d, L, F)
     D = d // H
     hoffs = np.asarray(hist_offsets, dtype=np.int64)
@@ -285,7 +287,7 @@ def rank_hidden(blob, d, H, L, F, cache, hist_offsets, cand_emb, cand_offsets,
                 p = np.exp(s - m)
                 p = p / p.sum(axis=1, keepdims=True)
                 o[j] = p[:, :-1] @ Vh + p[:, -1:] * vs[j]
-            g = g + lin(o_in(o.transpose(1, 0, 2).reshape(kc_rows, d)), lw["Wo"], lw["bo"])
+            g = g + lin(o.transpose(1, 0, 2).reshape(kc_rows, d), lw["Wo"], lw["bo"])
             g = g + ffn(g, lw, lin)
         hidden[rows] = g
     return hidden

@@ -104,7 +104,8 @@ __device__ __forceinline__ float quad_sum(float v) {
 // (stride 3d, own key and value at +d, +2d).  CAUSAL = true: encode; queries
 // are history rows of qsrc = query rows (stride d), own keys in the cache.
 // MXO: the output goes out as MXFP8 (codes in `out`, one E8M0 byte per
-// 32-value block in `out_scales`) for the fp8 projection variant; else fp16.
+// 32-value block in `out_scales`), encoded from the fp32 values, for the fp8
+// projection variant; else fp16.
 template <bool CAUSAL, int kQG, bool MXO = false>
 __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
     const bf16* __restrict__ qsrc, int64_t qstride, void* __restrict__ out,
@@ -380,16 +381,16 @@ __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
                 *reinterpret_cast<h4*>(op + eb * 16 + 4 * g) = v;
             }
         } else {
-            // The fp16 values the unfused path stores, then encoded as the
-            // standalone MXFP8 encoder would encode them: a head's 64 values
-            // are blocks 2h and 2h + 1 of the row (e < 32 and e >= 32, i.e.
-            // eb < 2 and eb >= 2), each spread over the query's four lanes.
+            // MXFP8 encoding of the normalised fp32 values (no narrower
+            // intermediate): a head's 64 values are blocks 2h and 2h + 1 of
+            // the row (e < 32 and e >= 32, i.e. eb < 2 and eb >= 2), each
+            // spread over the query's four lanes.
             float am[2] = {0.f, 0.f};
 #pragma unroll
             for (int eb = 0; eb < 4; ++eb)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    o[qg][eb][r] = (float)(f16)keep_f32(o[qg][eb][r] * inv);
+                    o[qg][eb][r] = keep_f32(o[qg][eb][r] * inv);
                     am[eb >> 1] = fmaxf(am[eb >> 1], fabsf(o[qg][eb][r]));
                 }
 #pragma unroll

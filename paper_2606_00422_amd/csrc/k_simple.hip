@@ -1,7 +1,8 @@
-// Reference-quality kernels: a tiled FMA GEMM with the projection epilogues,
-// and per-(row, head) attention for ranking and for history encoding.
-// They serve fp32 models (all arithmetic fp32) and are the baseline the MFMA
-// kernels are checked against.
+// Plain kernels: a tiled FMA GEMM with the projection epilogues, and
+// per-(row, head) attention for ranking and for history encoding.  They run
+// the fp32 models (all arithmetic fp32) and the shapes the MFMA kernels do
+// not take (head_dim 32).  Like every kernel here they are tested against
+// the CPU oracle.
 #include <cmath>
 
 #include "epilogue.h"
@@ -259,5 +260,11 @@ hipError_t launch_attn_encode_simple(const TKV* q, TA* o, int64_t rows, int64_t 
 UPR_INST(float, float)
 UPR_INST(bf16, f16)
 #undef UPR_INST
+// the fp8 projection variant's fallback attention: bf16 queries/keys/values
+// and cache, fp32 output for the MXFP8 encoder
+template hipError_t launch_attn_rank_simple<bf16, float>(const bf16*, float*, int64_t, int64_t,
+                                                         int, int, const int32_t*, const int32_t*,
+                                                         int, const bf16*, const bf16*, int64_t,
+                                                         hipStream_t);
 
 }  // namespace upr

@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <type_traits>
@@ -54,6 +55,10 @@ upr_status ok() {
     g_last_error.clear();
     return UPR_OK;
 }
+
+// Discards a HIP error left pending by the caller's earlier work, so that a
+// launch check of this call reports only this call's own failures.
+void clear_pending_error() { (void)hipGetLastError(); }
 
 // bf16 storage (tokens, cache): UPR_BF16 and its fp8-projection variant
 bool bf16_family(int32_t dt) { return dt == UPR_BF16 || dt == UPR_BF16_MXFP8; }
@@ -206,11 +211,25 @@ upr_status check_workspace(void* ws, size_t ws_bytes, size_t need) {
             return fail(UPR_ERR_HIP, "%s failed: %s", #__VA_ARGS__, hipGetErrorString(e_));     \
     } while (0)
 
+// Testing hook.  With UPR_STOP_AFTER=n in the environment, an encode or
+// rank call enqueues only the first n launches of its sequence (those made
+// through UPR_LAUNCH) and returns UPR_OK, leaving the workspace as they
+// wrote it, so that a test can check one stage at a time against the oracle
+// on the GPU's own inputs of that stage.  Unset: no limit.
+thread_local int64_t g_launches_left = -1;
+
+void arm_stop_hook() {
+    const char* e = std::getenv("UPR_STOP_AFTER");
+    g_launches_left = (e != nullptr && *e != '\0') ? std::strtoll(e, nullptr, 10) : -1;
+}
+
 // Launch with a named timing scope (a no-op unless profiling is enabled).
 #define UPR_LAUNCH(name, ...)                                                                   \
     do {                                                                                        \
+        if (g_launches_left == 0) return UPR_OK;                                                \
         ProfScope ps_(name, s);                                                                 \
         UPR_HIP(__VA_ARGS__);                                                                   \
+        if (g_launches_left > 0) --g_launches_left;                                             \
     } while (0)
 
 size_t elem_size(const upr_config& c) { return bf16_family(c.dtype) ? 2 : 4; }
@@ -268,8 +287,8 @@ void mx_quantize_host(const float* x, int64_t rows, int k, uint8_t* codes, uint8
 
 // Candidate layers of the fp8-projection variant: the bf16 sequence with
 // MXFP8 projection operands (LayerNorms write MXFP8 directly, the attention
-// kernel encodes its fp16-rounded output, the FFN-up GEMM writes its GELU
-// output as MXFP8).
+// kernel encodes its fp32 output, the FFN-up GEMM writes its GELU output as
+// MXFP8).
 static upr_status rank_layers_mx(const upr_model* m, const upr_kv_cache* cache,
                                  const upr_segments* hist, const bf16* cand_emb,
                                  const upr_segments* cand, const RankPlan& p, char* ws,
@@ -281,7 +300,7 @@ static upr_status rank_layers_mx(const upr_model* m, const upr_kv_cache* cache,
     uint8_t* ac = reinterpret_cast<uint8_t*>(ws + p.off_a);
     uint8_t* asc = ac + align256((size_t)R * d);
     bf16* qkv = reinterpret_cast<bf16*>(ws + p.off_qkv);
-    f16* o = reinterpret_cast<f16*>(ws + p.off_o);
+    float* o32 = reinterpret_cast<float*>(ws + p.off_o);
     uint8_t* hc = reinterpret_cast<uint8_t*>(ws + p.off_h);
     uint8_t* hsc = hc + align256((size_t)R * F);
     const float qscale = 1.4426950408889634f / std::sqrt((float)D);
@@ -339,11 +358,12 @@ static upr_status rank_layers_mx(const upr_model* m, const upr_kv_cache* cache,
                                                         p.work_items, p.attn_tile, ck, cv,
                                                         cache->capacity_rows, s));
         } else {
+            // fp32 attention output, then the MXFP8 encoder
             UPR_LAUNCH("rank.attn",
-                       launch_attn_rank_simple<bf16, f16>(qkv, o, R, p.row0, H, D, cand->offsets_dev,
-                                                          hist->offsets_dev, cand->num_users, ck, cv,
-                                                          cache->capacity_rows, s));
-            UPR_LAUNCH("rank.quant_o", launch_mx_quantize<f16>(o, R, d, ac, asc, s));
+                       launch_attn_rank_simple<bf16, float>(qkv, o32, R, p.row0, H, D, cand->offsets_dev,
+                                                            hist->offsets_dev, cand->num_users, ck, cv,
+                                                            cache->capacity_rows, s));
+            UPR_LAUNCH("rank.quant_o", launch_mx_quantize<float>(o32, R, d, ac, asc, s));
         }
         Epilogue r = resid_epilogue(w.bo, fuse ? w.ln2_g : nullptr, w.ln2_b);
         if (l == 0) r.resid_src = cand_emb + p.row0 * d;
@@ -820,6 +840,8 @@ upr_status upr_encode_user(const upr_model* m, const void* hist_emb, const upr_s
     st = check_workspace(ws, ws_bytes, p.bytes);
     if (st != UPR_OK) return st;
     if (p.rows == 0) return ok();
+    clear_pending_error();
+    arm_stop_hook();
     hipStream_t s = static_cast<hipStream_t>(stream);
     char* w = static_cast<char*>(ws);
     st = bf16_family(m->cfg.dtype)
@@ -856,6 +878,8 @@ upr_status upr_rank_candidates(const upr_model* m, const upr_kv_cache* cache,
     st = check_workspace(ws, ws_bytes, p.bytes);
     if (st != UPR_OK) return st;
     if (p.rows == 0) return ok();
+    clear_pending_error();
+    arm_stop_hook();
     hipStream_t s = static_cast<hipStream_t>(stream);
     char* w = static_cast<char*>(ws);
     upr::RankOut out;
@@ -986,6 +1010,8 @@ upr_status upr_rank_actions(const upr_model* m, const upr_heads* hd, const upr_k
     for (int c = 0; c < hd->C; ++c) out.uw.u[c] = utility_weights[c];
     out.probs = probs;
     out.util = utility;
+    clear_pending_error();
+    arm_stop_hook();
     hipStream_t s = static_cast<hipStream_t>(stream);
     char* w = static_cast<char*>(ws);
     st = bf16_family(m->cfg.dtype)
@@ -1012,6 +1038,7 @@ upr_status upr_topk_by_utility(const float* utility, const upr_segments* cand, i
     if (cand->num_users == 0) return ok();
     if (!topk_rows) return fail(UPR_ERR_NULL, "topk_rows is NULL");
     if (cl > cf && !utility) return fail(UPR_ERR_NULL, "utility is NULL");
+    clear_pending_error();
     hipStream_t s = static_cast<hipStream_t>(stream);
     {
         upr::ProfScope ps("topk", s);
@@ -1043,6 +1070,7 @@ upr_status upr_mx_quantize(const void* x, int32_t in_type, int64_t rows, int32_t
                     (long long)rows, k);
     if (rows == 0) return ok();
     if (!x || !codes || !scales) return fail(UPR_ERR_NULL, "x, codes or scales is NULL");
+    clear_pending_error();
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e;
     {
@@ -1072,6 +1100,7 @@ upr_status upr_mx_linear(const uint8_t* a_codes, const uint8_t* a_scales, const 
     r.bias = bias;
     r.resid = out;
     r.ldr = N;
+    clear_pending_error();
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e;
     {

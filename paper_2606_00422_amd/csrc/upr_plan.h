@@ -102,7 +102,10 @@ inline RankPlan plan_rank(const upr_config& c, int U, const int32_t* coffs, int 
     p.off_g = o; o = align256(o + R * d * 4);
     p.off_a = o; o = align256(o + R * d * es);
     p.off_qkv = o; o = align256(o + R * 3 * d * es);
-    p.off_o = o; o = align256(o + R * d * es);
+    // (the fp8 variant's fallback attention, head_dim 32, writes fp32 here
+    // before the MXFP8 encoder reads it)
+    const size_t o_es = c.dtype == UPR_BF16_MXFP8 ? 4 : es;
+    p.off_o = o; o = align256(o + R * d * o_es);
     p.off_h = o; o = align256(o + R * std::max<size_t>(F, (size_t)head_cols) * es);
     p.off_work = o; o = align256(o + (size_t)p.work_items * 4 * sizeof(int32_t));
     p.bytes = o;
@@ -135,8 +138,8 @@ hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
                             hipStream_t s);
 
 // The same with the output as MXFP8 (codes [rows, H*64], one E8M0 scale byte
-// per 32-value block [rows, H*2]), encoded from the fp16 values the call
-// above writes: the fp8 projection variant's input of the O projection.
+// per 32-value block [rows, H*2]), encoded from the normalised fp32 values:
+// the fp8 projection variant's input of the O projection.
 hipError_t launch_attn_rank_mx(const bf16* qkv, uint8_t* codes, uint8_t* scales, int64_t row0,
                                int H, int D, const int32_t* hist_offsets, const int32_t* work,
                                int64_t items, int tile, const bf16* cache_k, const bf16* cache_v,

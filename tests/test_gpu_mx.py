@@ -193,3 +193,238 @@ def test_mxfp8_action_heads_follow_the_rule():
     assert np.abs(g - rule).max() <= 0.25 * MX_MAX      # sigmoid slope <= 1/4
     for K in (1, 5, 64):
         _check_topk(run, g_util[: max(rows, 1)], K)
+
+
+# ---------------------------------------------------------------------------
+# Stage-by-stage split check of the fp8 ranking pass
+# ---------------------------------------------------------------------------
+#
+# UPR_STOP_AFTER=n makes a rank call stop after the first n launches of its
+# sequence, leaving the workspace as they wrote it.  Each stage is then
+# checked element by element against the oracle evaluated on the GPU's own
+# inputs of that stage (the workspace left by the stage before):
+#
+# * an MXFP8 encoding (LN1 / LN2 / attention / GELU outputs) must be the
+#   oracle's encoding (oracle.mx_quantize) of some value within delta of the
+#   oracle's float64 pre-quantization value, where delta bounds the GPU's own
+#   error in computing that value; the block exponent likewise from the block
+#   maximum.  Away from E4M3 rounding boundaries that is bit-exactness; the
+#   test reports how many codes needed the margin;
+# * a projection output must lie within 2.5e-4 (|A| |W|^T) of the float64
+#   product of the decoded operands (plus the rounding of its own storage).
+
+def _ws_layout(R, d, F, items):
+    a256 = lambda x: (x + 255) & ~255
+    o = 0
+    lay = {"g": o}
+    o = a256(o + R * d * 4)
+    lay["a"], lay["a_s"] = o, o + a256(R * d)
+    o = a256(o + R * d * 2)
+    lay["qkv"] = o
+    o = a256(o + R * 3 * d * 2)
+    lay["o"] = o
+    o = a256(o + R * d * 4)
+    lay["h"], lay["h_s"] = o, o + a256(R * F)
+    o = a256(o + R * F * 2)
+    lay["work"] = o
+    lay["bytes"] = a256(o + items * 16)
+    return lay
+
+
+def _mx_sequence(d, L, mfma_attn):
+    seq = ["init_ln1"] + (["worklist"] if mfma_attn else [])
+    for l in range(L):
+        seq += (["ln1"] if l > 0 else []) + ["gemm_qkv", "attn"] + ([] if mfma_attn else ["quant_o"])
+        seq += ["gemm_o"] + ([] if d <= 512 else ["ln2"]) + ["gemm_up", "gemm_down"]
+    return seq + ["score_head"]
+
+
+def _check_encoding(codes, scales, x, delta, label, max_margin_frac):
+    rows, K = x.shape
+    xb = x.reshape(rows, K // 32, 32)
+    db = np.broadcast_to(delta, x.shape).reshape(rows, K // 32, 32)
+    amax = np.abs(xb).max(-1)
+    dmax = db.max(-1)
+    e_gpu = scales.astype(np.int64) - 127
+    e_lo = oracle.mx_block_exponent(np.maximum(amax - dmax, 0.0))
+    e_hi = oracle.mx_block_exponent(amax + dmax)
+    bad_e = (e_gpu < e_lo) | (e_gpu > e_hi)
+    assert not bad_e.any(), f"{label}: {bad_e.sum()} block exponents outside the admissible range"
+    sc = np.exp2(e_gpu.astype(np.float64))[..., None]
+    lo = oracle.e4m3_value(oracle.e4m3_round_codes((xb - db) / sc))
+    hi = oracle.e4m3_value(oracle.e4m3_round_codes((xb + db) / sc))
+    v = oracle.e4m3_value(codes.reshape(rows, K // 32, 32))
+    bad = (v < lo) | (v > hi)
+    assert not bad.any(), (f"{label}: {bad.sum()} of {v.size} codes are no rounding of a value "
+                           f"within delta of the oracle's")
+    exact_c, exact_s = oracle.mx_quantize(x)
+    margin = float(np.mean(codes != exact_c))
+    say(f"[gpu]   {label}: codes equal to the oracle's own encoding except {margin:.2e} "
+        f"(block exponents except {float(np.mean(scales != exact_s)):.2e})")
+    assert margin <= max_margin_frac, f"{label}: {margin:.3e} of the codes needed the margin"
+
+
+def _check_linear(out, ref, bound, label):
+    err = np.abs(out - ref)
+    assert np.all(err <= bound), (f"{label}: max err {err.max():.3e}, worst ratio "
+                                  f"{(err / bound).max():.3f}")
+    say(f"[gpu]   {label}: max err/bound {(err / bound).max():.3f}")
+
+
+def _ln(x, g, b, eps=1e-5):
+    mu = x.mean(-1, keepdims=True)
+    var = ((x - mu) ** 2).mean(-1, keepdims=True)
+    return (x - mu) / np.sqrt(var + eps) * g + b
+
+
+def _ln_delta(y):
+    # fp32 LayerNorm on the GPU: mean, variance and 1/sqrt each a few fp32
+    # roundings over at most 1024 values; 2e-5 relative covers them
+    return 2e-5 * (np.abs(y) + 1.0)
+
+
+MX_STAGE_CASES = [
+    # (hist lens, cand lens, d, H, L, F): MFMA attention (head_dim 64) with the
+    # fused LN2; the fallback attention (head_dim 32) with its fp32 output and
+    # the device encoder; d = 768 with the unfused LN2 row kernel
+    ([300, 0, 129], [200, 67, 513], 512, 8, 2, 1024),
+    ([90, 260], [150, 71], 256, 8, 2, 512),
+    ([70, 33], [65, 140], 768, 12, 1, 512),
+]
+
+
+@pytest.mark.parametrize("case", range(len(MX_STAGE_CASES)))
+def test_mxfp8_stages_split_check(case, monkeypatch):
+    hl, kl, d, H, L, F = MX_STAGE_CASES[case]
+    inp = make_inputs(hl, kl, d, H, L, F, dtype="bf16", seed=500 + case, variant="perturbed")
+    D = d // H
+    mfma_attn = D == 64
+    say(f"[gpu] mxfp8 stages case {case}: d={d} H={H} L={L} F={F} Kc={inp.cand_offsets[-1]}")
+    run = GpuRun(inp, model_dtype="bf16_mxfp8")
+    run.encode()
+    layers, final = oracle.unpack_weights(inp.weights, d, L, F)
+    R = int(inp.cand_offsets[-1])
+    cache = run.cache_np()
+    hd = torch.from_numpy(run.hoff).cuda()
+    cd = torch.from_numpy(run.coff).cuda()
+    need = upr.upr_rank_workspace_bytes(run.model.handle, upr.segments(run.hoff, hd),
+                                        upr.segments(run.coff, cd))
+    tile = 128 if H * sum(-(-k // 128) for k in kl) >= 512 else 64
+    lay = _ws_layout(R, d, F, H * sum(-(-k // tile) for k in kl))
+    assert lay["bytes"] == need, "workspace layout of the test differs from the library's"
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    seq = _mx_sequence(d, L, mfma_attn)
+
+    # the launch sequence the test walks is the library's
+    upr.upr_profile_enable(True)
+    run.model.rank(run.cache, run.hoff, hd, run.C, run.coff, cd, run.scores, ws=ws)
+    prof = upr.upr_profile_read()
+    upr.upr_profile_enable(False)
+    counts = {}
+    for s_ in seq:
+        counts["rank." + s_] = counts.get("rank." + s_, 0) + 1
+    assert {k: v[0] for k, v in prof.items()} == counts
+
+    def snap(n):
+        monkeypatch.setenv("UPR_STOP_AFTER", str(n))
+        ws.fill_(0)
+        run.model.rank(run.cache, run.hoff, hd, run.C, run.coff, cd, run.scores, ws=ws)
+        torch.cuda.synchronize()
+        monkeypatch.delenv("UPR_STOP_AFTER")
+        b = ws.cpu()
+        view = lambda off, n_, dt: b[off:off + n_ * torch.empty(0, dtype=dt).element_size()].view(dt)
+        return {
+            "g": view(lay["g"], R * d, torch.float32).numpy().reshape(R, d).astype(np.float64),
+            "a": view(lay["a"], R * d, torch.uint8).numpy().reshape(R, d).copy(),
+            "a_s": view(lay["a_s"], R * d // 32, torch.uint8).numpy().reshape(R, d // 32).copy(),
+            "qkv": view(lay["qkv"], R * 3 * d, torch.bfloat16).float().numpy().reshape(R, 3 * d)
+                   .astype(np.float64),
+            "o": view(lay["o"], R * d, torch.float32).numpy().reshape(R, d).astype(np.float64),
+            "h": view(lay["h"], R * F, torch.uint8).numpy().reshape(R, F).copy(),
+            "h_s": view(lay["h_s"], R * F // 32, torch.uint8).numpy().reshape(R, F // 32).copy(),
+            "scores": run.scores.cpu().numpy()[:R].astype(np.float64),
+        }
+
+    Wmx = lambda W: oracle.mx_dequantize(*oracle.mx_quantize(W))
+    qscale = np.log2(np.e) / np.sqrt(D)
+    tokens = inp.cand_emb.astype(np.float64)
+    ho, co = inp.hist_offsets, inp.cand_offsets
+    g_prev = tokens                      # the residual before the current stage
+    prev = None
+    layer = -1
+    for n, stage in enumerate(seq, start=1):
+        cur = snap(n)
+        if stage in ("init_ln1", "ln1"):
+            layer += 1
+            lw = layers[layer]
+            src = tokens if stage == "init_ln1" else cur["g"]
+            x = _ln(src, lw["ln1_g"], lw["ln1_b"])
+            _check_encoding(cur["a"], cur["a_s"], x, _ln_delta(x), f"L{layer} {stage}", 1e-3)
+        elif stage == "gemm_qkv":
+            A = oracle.mx_dequantize(cur["a"], cur["a_s"])
+            W = np.concatenate([Wmx(lw["Wq"]), Wmx(lw["Wk"]), Wmx(lw["Wv"])])
+            b = np.concatenate([lw["bq"], lw["bk"], lw["bv"]])
+            cs = np.concatenate([np.full(d, qscale), np.ones(2 * d)])
+            ref = (A @ W.T + b) * cs
+            bound = 2.5e-4 * (np.abs(A) @ np.abs(W).T) * cs + 2.0 ** -8 * np.abs(ref) + 1e-6
+            _check_linear(cur["qkv"], ref, bound, f"L{layer} qkv")
+        elif stage == "attn":
+            qkv = cur["qkv"]
+            o = np.zeros((R, d))
+            spread = np.zeros((R, d))
+            for u in range(inp.U):
+                rows = slice(co[u], co[u + 1])
+                for j in range(H):
+                    sl = slice(j * D, (j + 1) * D)
+                    q = qkv[rows, sl]
+                    ks, vs = qkv[rows, d + j * D: d + (j + 1) * D], qkv[rows, 2 * d + j * D: 2 * d + (j + 1) * D]
+                    Kh, Vh = cache[layer, 0, j, ho[u]:ho[u + 1]], cache[layer, 1, j, ho[u]:ho[u + 1]]
+                    s = np.concatenate([q @ Kh.T, np.sum(q * ks, 1, keepdims=True)], 1)  # base-2 logits
+                    p = np.exp2(s - s.max(1, keepdims=True))
+                    p /= p.sum(1, keepdims=True)
+                    oo = p[:, :-1] @ Vh + p[:, -1:] * vs
+                    o[rows, sl] = oo
+                    # |o_gpu - o| <= 2^-8 sum_t p_t |v_t - o| (bf16 probabilities)
+                    spread[rows, sl] = p[:, :-1] @ np.abs(Vh) + p[:, -1:] * np.abs(vs) + np.abs(oo)
+            delta = 2.0 ** -8 * spread + 1e-6
+            if mfma_attn:
+                _check_encoding(cur["a"], cur["a_s"], o, delta, f"L{layer} attention", 0.05)
+            else:
+                _check_linear(cur["o"], o, 1e-5 * spread + 1e-6, f"L{layer} attention (fp32)")
+        elif stage == "quant_o":
+            # the encoder's input is in the workspace: bit-exact
+            c, sc = oracle.mx_quantize(cur["o"])
+            np.testing.assert_array_equal(cur["a_s"], sc)
+            np.testing.assert_array_equal(cur["a"], c)
+        elif stage == "gemm_o":
+            A = oracle.mx_dequantize(prev["a"], prev["a_s"])
+            W = Wmx(lw["Wo"])
+            ref = g_prev + A @ W.T + lw["bo"]
+            _check_linear(cur["g"], ref, 2.5e-4 * (np.abs(A) @ np.abs(W).T) + 1e-6 * (1 + np.abs(ref)),
+                          f"L{layer} O projection")
+            g_prev = cur["g"]
+            if d <= 512:
+                x = _ln(cur["g"], lw["ln2_g"], lw["ln2_b"])
+                _check_encoding(cur["a"], cur["a_s"], x, _ln_delta(x), f"L{layer} LN2 (fused)", 1e-3)
+        elif stage == "ln2":
+            x = _ln(cur["g"], lw["ln2_g"], lw["ln2_b"])
+            _check_encoding(cur["a"], cur["a_s"], x, _ln_delta(x), f"L{layer} LN2", 1e-3)
+        elif stage == "gemm_up":
+            A = oracle.mx_dequantize(cur["a"], cur["a_s"])
+            W = Wmx(lw["W1"])
+            pre = A @ W.T + lw["b1"]
+            x = oracle.gelu_tanh(pre)
+            # GELU's slope is below 1.13; its fp32 evaluation adds ~1e-6 relative
+            delta = 1.13 * (2.5e-4 * (np.abs(A) @ np.abs(W).T) + 1e-6) + 1e-5 * np.abs(x)
+            _check_encoding(cur["h"], cur["h_s"], x, delta, f"L{layer} GELU", 0.05)
+        elif stage == "gemm_down":
+            A = oracle.mx_dequantize(cur["h"], cur["h_s"])
+            W = Wmx(lw["W2"])
+            ref = g_prev + A @ W.T + lw["b2"]
+            _check_linear(cur["g"], ref, 2.5e-4 * (np.abs(A) @ np.abs(W).T) + 1e-6 * (1 + np.abs(ref)),
+                          f"L{layer} FFN down")
+            g_prev = cur["g"]
+        elif stage == "score_head":
+            ref = oracle.score_head(cur["g"], final)
+            _check_linear(cur["scores"], ref, 1e-4 * (1 + np.abs(ref)), "score head")
+        prev = cur

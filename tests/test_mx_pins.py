@@ -108,13 +108,6 @@ def test_all_zero_and_mixed_sign_blocks():
     assert s[0] == 127 and c[0] == m.e4m3_round_codes(300.0) and c[1] == 0x80
 
 
-def test_f16_round_matches_torch():
-    x = np.concatenate([RNG.standard_normal(20000) * np.exp2(RNG.integers(-20, 15, 20000)),
-                        [0.0, -0.0, 1.0 + 2.0 ** -11, 1.0 + 3 * 2.0 ** -11, 65504.0]])
-    ref = torch.tensor(x.astype(np.float32)).to(torch.float16).to(torch.float64).numpy()
-    np.testing.assert_array_equal(mx_oracle.f16_round(x), ref)
-
-
 def test_linear_mx_matches_torch_fp8_when_every_scale_is_one():
     """Blocks whose largest magnitude is 300 take scale 2^0, so the MXFP8
     values are plain E4M3 roundings: torch's float8_e4m3fn cast gives the
@@ -211,12 +204,119 @@ def test_mxfp8_rule_sensitivity():
         noisy = lambda x, W, b, f: f(x, W, b) * (1 + 1e-3 * rng.standard_normal((x.shape[0], W.shape[0])))
         real = uo._projection_rule
         try:
-            uo._projection_rule = lambda proj: ((lambda x, W, b: noisy(x, W, b, m.linear_mx)), m.f16_round)
+            uo._projection_rule = lambda proj: (lambda x, W, b: noisy(x, W, b, m.linear_mx))
             moved = oracle.rank(*args, proj="mxfp8")
-            uo._projection_rule = lambda proj: ((lambda x, W, b: noisy(x, W, b, uo.linear)), (lambda o: o))
+            uo._projection_rule = lambda proj: (lambda x, W, b: noisy(x, W, b, uo.linear))
             moved_exact = oracle.rank(*args)
         finally:
             uo._projection_rule = real
         assert rms(moved - base) <= 0.07 and np.abs(moved - base).max() <= 0.25
         assert rms(moved - base) > 5e-3                       # it does move: the rounding is discontinuous
         assert rms(moved_exact - exact) < 0.1 * rms(moved - base)
+
+
+# ---------------------------------------------------------------------------
+# The composition, rebuilt from torch operations
+# ---------------------------------------------------------------------------
+
+def _torch_e4m3_round(s):
+    """s rounded to E4M3 values, written independently of the oracle: three
+    fraction bits by the add-and-subtract method in float64 (adding
+    c = 1.5 * 2^(49 + e) puts the sum's last significand bit at 2^(e - 3),
+    and float64 addition rounds to nearest, ties to even), exponents below
+    -6 sharing the subnormal step 2^-9, magnitudes saturated at 448."""
+    a = s.abs()
+    _, ex = torch.frexp(a)                        # a = m 2^ex, m in [0.5, 1)
+    e = torch.clamp(ex - 1, min=-6).to(torch.float64)
+    c = 1.5 * torch.exp2(e + 49.0)
+    r = torch.clamp((a + c) - c, max=448.0)
+    return torch.copysign(r, s)
+
+
+def _torch_mx_round(x):
+    """x replaced by its MXFP8 values along the last axis: blocks of 32, scale
+    2^(floor(log2 max|v|) - 8) (2^-127 for an all-zero block), from
+    torch.frexp."""
+    K = x.shape[-1]
+    b = x.reshape(*x.shape[:-1], K // 32, 32)
+    amax = b.abs().amax(dim=-1)
+    _, ex = torch.frexp(amax)
+    e = torch.where(amax > 0, ex - 9, torch.full_like(ex, -127)).clamp(-127, 127)
+    sc = torch.exp2(e.to(torch.float64))[..., None]
+    return (_torch_e4m3_round(b / sc) * sc).reshape(x.shape)
+
+
+def _torch_mx_rank(inp, cache):
+    """One candidate pass of the fp8 projection rule from torch.nn.functional
+    pieces: LayerNorm, tanh GELU and softmax from torch, every projection
+    input and weight through _torch_mx_round, attention over the cached
+    history plus the candidate's own key; float64 elsewhere."""
+    import torch.nn.functional as Fn
+    from synth import blob_layout
+    d, H, L, Fd = inp.d, inp.H, inp.L, inp.F
+    D = d // H
+    w, pos = {}, 0
+    blob = torch.as_tensor(np.asarray(inp.weights, dtype=np.float64))
+    for name, shape, _ in blob_layout(d, L, Fd):
+        n = int(np.prod(shape))
+        w[name] = blob[pos:pos + n].reshape(shape)
+        pos += n
+    lin = lambda x, W, b: _torch_mx_round(x) @ _torch_mx_round(W).T + b
+    kv = torch.as_tensor(np.asarray(cache, dtype=np.float64))
+    Cm = torch.as_tensor(np.asarray(inp.cand_emb, dtype=np.float64))
+    ho, co = inp.hist_offsets, inp.cand_offsets
+    out = torch.full((Cm.shape[0],), float("nan"), dtype=torch.float64)
+    for u in range(inp.U):
+        g = Cm[co[u]:co[u + 1]]
+        if g.shape[0] == 0:
+            continue
+        lo, hi = int(ho[u]), int(ho[u + 1])
+        for l in range(L):
+            p = f"l{l}."
+            a = Fn.layer_norm(g, (d,), w[p + "ln1_g"], w[p + "ln1_b"], eps=1e-5)
+            q, k, v = (lin(a, w[p + "W" + t], w[p + "b" + t]) for t in "qkv")
+            heads = []
+            for j in range(H):
+                sl = slice(j * D, (j + 1) * D)
+                Kh, Vh = kv[l, 0, j, lo:hi], kv[l, 1, j, lo:hi]
+                logits = torch.cat([q[:, sl] @ Kh.T, (q[:, sl] * k[:, sl]).sum(-1, keepdim=True)], 1)
+                pr = torch.softmax(logits / np.sqrt(D), dim=-1)
+                heads.append(pr[:, :-1] @ Vh + pr[:, -1:] * v[:, sl])
+            g = g + lin(torch.cat(heads, 1), w[p + "Wo"], w[p + "bo"])
+            a2 = Fn.layer_norm(g, (d,), w[p + "ln2_g"], w[p + "ln2_b"], eps=1e-5)
+            g = g + lin(Fn.gelu(lin(a2, w[p + "W1"], w[p + "b1"]), approximate="tanh"),
+                        w[p + "W2"], w[p + "b2"])
+        z = Fn.layer_norm(g, (d,), w["lnf_g"], w["lnf_b"], eps=1e-5)
+        out[co[u]:co[u + 1]] = z @ w["w_score"].reshape(-1) + w["b_score"].reshape(())
+    return out.numpy()
+
+
+def test_torch_e4m3_rounding_agrees_with_torch_cast():
+    """The independent rounding above against torch's own float8_e4m3fn cast
+    on float32-representable values (no double rounding there), saturation
+    aside."""
+    x = _f32(np.concatenate([RNG.uniform(-448, 448, 20000), RNG.uniform(-0.05, 0.05, 20000)]))
+    ours = _torch_e4m3_round(torch.as_tensor(x)).numpy()
+    ref = torch.tensor(x).to(torch.float8_e4m3fn).to(torch.float64).numpy()
+    np.testing.assert_array_equal(ours, ref)
+
+
+def test_mxfp8_rank_matches_an_independent_composition():
+    """oracle.rank(proj="mxfp8") against the same forward pass assembled
+    from torch operations with an independently written MX rounding: every
+    quantization point (LN1 output, attention output, LN2 output, GELU
+    output, each weight), its axis and block and nothing else rounded.  Both
+    sides are float64 away from the E4M3 points, so they agree to rounding
+    order."""
+    import oracle
+    from synth import make_inputs
+    inp = make_inputs([37, 0, 70], [29, 6, 41], d=64, H=2, L=2, F=128, dtype="bf16", seed=23,
+                      variant="perturbed")
+    cache = oracle.encode(inp.weights, inp.d, inp.H, inp.L, inp.F, inp.hist_emb, inp.hist_offsets)
+    ref = _torch_mx_rank(inp, cache)
+    got = oracle.rank(inp.weights, inp.d, inp.H, inp.L, inp.F, cache, inp.hist_offsets,
+                      inp.cand_emb, inp.cand_offsets, proj="mxfp8")
+    np.testing.assert_allclose(got, ref, rtol=1e-9, atol=1e-9)
+    exact = oracle.rank(inp.weights, inp.d, inp.H, inp.L, inp.F, cache, inp.hist_offsets,
+                        inp.cand_emb, inp.cand_offsets)
+    assert np.abs(got - exact).max() > 1e-3          # the quantization is really there

@@ -24,8 +24,8 @@ MUTATIONS = {
                                      "causal = np.tril(np.ones((n, n), dtype=bool), -1) | (np.arange(n)[:, None] == 0)"),
     "mask lets candidates see each other": ("cand_row = (i >= n) & ((j < n) | (j == i))",
                                             "cand_row = (i >= n) & (j <= i)"),
-    "Wo transposed in rank": ("g = g + lin(o_in(o.transpose(1, 0, 2).reshape(kc_rows, d)), lw[\"Wo\"], lw[\"bo\"])",
-                              "g = g + lin(o_in(o.transpose(1, 0, 2).reshape(kc_rows, d)), lw[\"Wo\"].T, lw[\"bo\"])"),
+    "Wo transposed in rank": ("g = g + lin(o.transpose(1, 0, 2).reshape(kc_rows, d), lw[\"Wo\"], lw[\"bo\"])",
+                              "g = g + lin(o.transpose(1, 0, 2).reshape(kc_rows, d), lw[\"Wo\"].T, lw[\"bo\"])"),
     "value bias dropped in rank": ("vs = _split_heads(lin(a, lw[\"Wv\"], lw[\"bv\"]), H)",
                                    "vs = _split_heads(lin(a, lw[\"Wv\"], 0.0), H)"),
     "gelu constant": ("0.044715", "0.04715"),

@@ -83,6 +83,13 @@ def measured_traffic(kernel, workload):
     return round(rec["hbm_read_bytes"] + rec["hbm_write_bytes"])
 
 
+def traffic_provenance(kernel):
+    rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))[TRAFFIC_KEYS[kernel]]
+    return (f"profiles/traffic.json: rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE passes over "
+            f"{rec['source']} (sha1 {rec['source_sha1']}), each scaled by the same counter's "
+            f"reading for a plain device copy; replayed here while that source is unchanged")
+
+
 def path_flops(inp):
     d, F, L = inp.d, inp.F, inp.L
     R = float(inp.cand_offsets[-1] - inp.cand_offsets[0])
@@ -245,34 +252,49 @@ def mxfp8_rank(args, inp, kv, hs, cs, C, Kc, ev, stream, work):
             "kernels": kernels}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="u64_n1024_k2000", choices=sorted(WORKLOADS))
-    ap.add_argument("--user-reps", type=int, default=3, help="reps of the per-user latency pass")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--no-actions", action="store_true",
-                    help="skip the per-action heads + utility top-K measurement")
-    ap.add_argument("--no-mxfp8", action="store_true",
-                    help="skip the fp8-projection variant's measurement")
-    ap.add_argument("--flush-mall", action="store_true",
-                    help="write a 512 MiB scratch buffer before every rank step (evicts the "
-                         "256 MB MALL; for counter runs, not for the headline number)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this path has no "
-              "multi-GPU mode; per-GPU work is independent by user.", file=sys.stderr)
-        sys.exit(2)
+def encode_flops(inp):
+    """Algorithmic FLOPs of one upr_encode_user over the workload's histories:
+    every layer's Q/K/V projection (the cache), and for all but the last
+    layer the causal attention (q.k and p.v over the n(n+1)/2 visible
+    pairs), the output projection and the FFN; the last layer stops once its
+    keys and values are in the cache."""
+    d, F, L = inp.d, inp.F, inp.L
+    n = inp.hist_lens.astype(np.float64)
+    per_layer_qkv = 6.0 * d * d * n.sum()
+    per_layer_rest = (2.0 * d * d + 4.0 * d * F) * n.sum() + 2.0 * d * np.sum(n * (n + 1))
+    return L * per_layer_qkv + (L - 1) * per_layer_rest
 
+
+def dominant_roofline(prof, work, workload):
+    dom = max((n for n in prof if n in work), key=lambda n: prof[n][1])
+    bound, amount = work[dom]
+    avg_s = prof[dom][1] / prof[dom][0] * 1e-3
+    traffic = measured_traffic(dom, workload)
+    if bound == "mfma":
+        achieved = amount / avg_s / 1e12
+        roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
+                "peak": PEAK_MFMA_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_MFMA_TFLOPS, 4), "traffic": traffic}
+    else:
+        achieved = amount / avg_s / 1e9
+        roof = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
+                "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic}
+    roof["work_per_launch"] = amount
+    roof["avg_launch_ms"] = round(avg_s * 1e3, 5)
+    roof["traffic_from"] = (traffic_provenance(dom) if traffic is not None else
+                            "null: no counter record for this kernel source and workload")
+    return roof
+
+
+def measure(name, args, full):
+    """One workload: encode once (timed), then `args.steps` timed rank steps,
+    then the same steps again with per-kernel HIP events.  `full` adds the
+    single-user latency passes and the variant measurements."""
     import torch
     from paper_2606_00422_amd import upr
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    torch.cuda.set_device(0)
-    inp = make_workload(args.workload, seed=args.seed)
+    inp = make_workload(name, seed=args.seed)
     cfg = upr.make_config(inp.d, inp.H, inp.L, inp.F, inp.dtype)
     model = upr.Model(cfg, inp.weights)
     tdt = torch.bfloat16 if inp.dtype == "bf16" else torch.float32
@@ -305,12 +327,15 @@ def main():
     ev = lambda: torch.cuda.Event(enable_timing=True)
     encode()
     torch.cuda.synchronize()
-    e0, e1 = ev(), ev()
-    e0.record()
-    encode()
-    e1.record()
-    torch.cuda.synchronize()
-    encode_ms = e0.elapsed_time(e1)
+    enc = []
+    for _ in range(3):
+        e0, e1 = ev(), ev()
+        e0.record()
+        encode()
+        e1.record()
+        torch.cuda.synchronize()
+        enc.append(e0.elapsed_time(e1))
+    encode_ms = float(np.median(enc))
 
     for _ in range(args.warmup):
         rank()
@@ -325,7 +350,7 @@ def main():
     torch.cuda.synchronize()
     ms = evs[0].elapsed_time(evs[-1]) / args.steps
     per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
-    assert bool(torch.isfinite(scores[:Kc]).all()), "non-finite scores"
+    assert bool(torch.isfinite(scores[:Kc]).all()), f"{name}: non-finite scores"
 
     # profiled pass over the same steps: per-kernel HIP events on the stream
     upr.upr_profile_enable(True)
@@ -337,31 +362,41 @@ def main():
 
     work = kernel_work(inp)
     kernels = {}
-    for name, (launches, total) in sorted(prof.items()):
+    for kname, (launches, total) in sorted(prof.items()):
         avg = total / launches
         entry = {"launches_per_step": launches / args.steps, "avg_ms": round(avg, 5)}
-        if name in work:
-            bound, amount = work[name]
+        if kname in work:
+            bound, amount = work[kname]
             if bound == "mfma":
                 entry["tflops"] = round(amount / (avg * 1e-3) / 1e12, 2)
             else:
                 entry["gbs"] = round(amount / (avg * 1e-3) / 1e9, 1)
-        kernels[name] = entry
-    dom = max((n for n in prof if n in work), key=lambda n: prof[n][1])
-    bound, amount = work[dom]
-    avg_s = prof[dom][1] / prof[dom][0] * 1e-3
-    if bound == "mfma":
-        achieved = amount / avg_s / 1e12
-        roof = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
-                "peak": PEAK_MFMA_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_MFMA_TFLOPS, 4),
-                "traffic": measured_traffic(dom, args.workload)}
-    else:
-        achieved = amount / avg_s / 1e9
-        roof = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
-                "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBS, 4),
-                "traffic": measured_traffic(dom, args.workload)}
+        kernels[kname] = entry
+    flops = path_flops(inp)
+    eflops = encode_flops(inp)
+    res = {
+        "ms_per_step": round(ms, 4),
+        "value": round(Kc / (ms * 1e-3), 1),
+        "unit": "candidate scores/s",
+        "config": {"workload": name, "users": inp.U, "flush_mall": bool(args.flush_mall),
+                   "history_rows": T, "candidate_rows": Kc, "d_model": inp.d,
+                   "heads": inp.H, "layers": inp.L, "d_ff": inp.F},
+        "path_tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+        "path_mfma_frac": round(flops / (ms * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
+        "step_ms": {"p10": round(float(np.percentile(per_step, 10)), 4),
+                    "p50": round(float(np.percentile(per_step, 50)), 4),
+                    "p90": round(float(np.percentile(per_step, 90)), 4)},
+        "roofline": dominant_roofline(prof, work, name),
+        "encode_ms": round(encode_ms, 3),
+        "encode_roofline": {"bound": "mfma", "flops": eflops,
+                            "achieved": round(eflops / (encode_ms * 1e-3) / 1e12, 2),
+                            "peak": PEAK_MFMA_TFLOPS, "unit": "TFLOP/s",
+                            "frac": round(eflops / (encode_ms * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4)},
+        "kernels": kernels,
+    }
+    if not full:
+        model.close()
+        return res, inp
 
     # single-user calls (sub-range of the packed buffers), per-call latency
     lat = []
@@ -403,44 +438,76 @@ def main():
         del g
     glat = np.array(glat) if glat else np.array([np.nan])
 
-    flops = path_flops(inp)
-
     def pct(v, q):          # null when the pass was skipped (JSON has no NaN)
         return None if np.all(np.isnan(v)) else round(float(np.nanpercentile(v, q)), 4)
 
+    res["user_latency_ms"] = {"p50": pct(lat, 50), "p90": pct(lat, 90),
+                              "calls": int(np.sum(~np.isnan(lat)))}
+    res["user_latency_graph_ms"] = {"p50": pct(glat, 50), "p90": pct(glat, 90),
+                                    "replays": int(np.sum(~np.isnan(glat)))}
+    if not args.no_actions:
+        res["actions_topk"] = actions_topk(args, inp, model, kv, hs, cs, C, Kc, ev, stream)
+    if not args.no_mxfp8 and inp.dtype == "bf16" and inp.d % 256 == 0 and inp.F % 128 == 0:
+        res["mxfp8"] = mxfp8_rank(args, inp, kv, hs, cs, C, Kc, ev, stream, work)
+    model.close()
+    return res, inp
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="u64_n1024_k2000", choices=sorted(WORKLOADS))
+    ap.add_argument("--others", default="u16_n256_k1000,ragged_u64,u8_n8192_k4096",
+                    help="comma-separated workloads measured after the headline, reported in "
+                         "the same line under 'workloads' ('' for none)")
+    ap.add_argument("--user-reps", type=int, default=3, help="reps of the per-user latency pass")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-actions", action="store_true",
+                    help="skip the per-action heads + utility top-K measurement")
+    ap.add_argument("--no-mxfp8", action="store_true",
+                    help="skip the fp8-projection variant's measurement")
+    ap.add_argument("--flush-mall", action="store_true",
+                    help="write a 512 MiB scratch buffer before every rank step (evicts the "
+                         "256 MB MALL; for counter runs, not for the headline number)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): this path has no "
+              "multi-GPU mode; per-GPU work is independent by user.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    print(f"[bench] {args.workload}: {args.steps} steps after {args.warmup} warmup",
+          file=sys.stderr, flush=True)
+    head, inp = measure(args.workload, args, full=True)
+    others = {}
+    for name in [w for w in args.others.split(",") if w and w != args.workload]:
+        print(f"[bench] {name}", file=sys.stderr, flush=True)
+        torch.cuda.empty_cache()
+        res, _ = measure(name, args, full=False)
+        others[name] = res
     out = {
         "metric": "candidate scores/sec (1 GPU)",
-        "value": round(Kc / (ms * 1e-3), 1),
-        "unit": "candidate scores/s",
+        "value": head.pop("value"),
+        "unit": head.pop("unit"),
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms, 4),
+        "ms_per_step": head.pop("ms_per_step"),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16+fp16" if inp.dtype == "bf16" else "f32",
         "data": "synthetic",
-        "config": {"workload": args.workload, "users": inp.U, "flush_mall": bool(args.flush_mall),
-                   "history_rows": T, "candidate_rows": Kc, "d_model": inp.d,
-                   "heads": inp.H, "layers": inp.L, "d_ff": inp.F},
-        "path_tflops": round(flops / (ms * 1e-3) / 1e12, 2),
-        "path_mfma_frac": round(flops / (ms * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
-        "step_ms": {"p10": round(float(np.percentile(per_step, 10)), 4),
-                    "p50": round(float(np.percentile(per_step, 50)), 4),
-                    "p90": round(float(np.percentile(per_step, 90)), 4)},
-        "user_latency_ms": {"p50": pct(lat, 50), "p90": pct(lat, 90),
-                            "calls": int(np.sum(~np.isnan(lat)))},
-        "user_latency_graph_ms": {"p50": pct(glat, 50), "p90": pct(glat, 90),
-                                  "replays": int(np.sum(~np.isnan(glat)))},
-        "encode_ms": round(encode_ms, 3),
-        "roofline": roof,
-        "kernels": kernels,
+        "config": head.pop("config"),
+        "roofline": head.pop("roofline"),
     }
-    if not args.no_actions:
-        out["actions_topk"] = actions_topk(args, inp, model, kv, hs, cs, C, Kc, ev, stream)
-    if not args.no_mxfp8 and inp.dtype == "bf16" and inp.d % 256 == 0 and inp.F % 128 == 0:
-        out["mxfp8"] = mxfp8_rank(args, inp, kv, hs, cs, C, Kc, ev, stream, work)
+    out.update(head)
+    out["workloads"] = others
     if not args.no_cpu_baseline:
+        print("[bench] cpu baseline", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(inp)
     print(json.dumps(out), flush=True)
-    model.close()
 
 
 if __name__ == "__main__":

@@ -19,9 +19,14 @@
  *   - `stream` is a hipStream_t passed as void*; NULL means the null stream.
  *     encode/rank enqueue work and return without synchronising.  A fault in
  *     a kernel surfaces at the caller's next synchronisation.
- *   - Arguments are validated on the host before anything is enqueued.  On a
- *     non-UPR_OK return nothing has been enqueued and no output byte has been
- *     written; upr_last_error() then gives a description (thread-local).
+ *   - Arguments are validated on the host before anything is enqueued.  A
+ *     validation failure (any status other than UPR_ERR_HIP) means nothing
+ *     has been enqueued and no output byte has been written.  UPR_ERR_HIP
+ *     reports a failed HIP call or kernel launch; kernels of the same call
+ *     enqueued before it may still run and write the call's outputs and
+ *     workspace.  A HIP error left pending by the caller's earlier work is
+ *     cleared at entry, not reported.  upr_last_error() gives a description
+ *     of the last failure (thread-local).
  *   - Row segments: offsets are int32, num_users+1 entries, non-decreasing,
  *     offsets[0] >= 0.  User u owns packed rows offsets[u] .. offsets[u+1]-1.
  *     offsets[0] > 0 is allowed (a call on a sub-range of a shared buffer).
@@ -67,7 +72,9 @@ typedef enum { UPR_F32 = 0, UPR_BF16 = 1, UPR_BF16_MXFP8 = 2 } upr_dtype;
  *             same peak rate, 3 more significand bits); the residual stream,
  *             normalisation statistics, softmax and every accumulation are
  *             fp32.  Activations entering the projections must stay within
- *             the fp16 range (|x| < 65504).
+ *             the fp16 range (|x| < 65504).  This is not checked: a value
+ *             beyond it becomes an fp16 infinity, and the scores of the rows
+ *             it reaches come out non-finite, never silently finite.
  *   UPR_BF16_MXFP8: the UPR_BF16 model (same weight blob, tokens and cache;
  *             encode unchanged) whose ranking layers run their four
  *             projections (Q/K/V, O, FFN up, FFN down) in FP8 (paper Sec. 3,

@@ -183,6 +183,30 @@ upr_status upr_rank_candidates(const upr_model* model, const upr_kv_cache* cache
                                const upr_segments* cand, float* scores,
                                void* ws, size_t ws_bytes, void* stream);
 
+/* Largest workspace upr_rank_candidates_noalloc can provide (bytes). */
+#define UPR_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * ranking as upr_rank_candidates, with the same arguments except the
+ * workspace, which comes from a fixed scratch array inside the library
+ * (UPR_NOALLOC_SCRATCH_BYTES per GPU, held from the first call on that GPU
+ * until the process ends).  Calls needing a larger workspace
+ * (upr_rank_workspace_bytes > UPR_NOALLOC_SCRATCH_BYTES; about 5,900
+ * candidate rows at d_model 512, d_ff 2048) fail with UPR_ERR_LIMIT before
+ * anything is enqueued.  The call allocates nothing (no hipMalloc, hipFree
+ * or allocating library routine); its first call on a GPU looks up that
+ * GPU's scratch address (UPR_ERR_HIP if the lookup fails).  Every call on one
+ * GPU shares that GPU's scratch array, whose contents are the last call's:
+ * calls that overlap in time on one GPU (several host threads, or streams
+ * that run concurrently) race and must be serialised by the caller.  Nothing
+ * in the array needs to start at any particular value.  While the diagnostic
+ * profiler (upr_profile_enable) is on, its timing events are created on
+ * first use. */
+upr_status upr_rank_candidates_noalloc(const upr_model* model, const upr_kv_cache* cache,
+                                       const upr_segments* hist, const void* cand_emb,
+                                       const upr_segments* cand, float* scores, void* stream);
+
 /* ---------------------------------------------------------------------
  * Per-action ranking heads and utility top-K (paper Sec. 3: the ranking
  * objective of Masked Action Modeling gives every action type c = 1..C its

@@ -852,10 +852,12 @@ upr_status upr_encode_user(const upr_model* m, const void* hist_emb, const upr_s
     return st == UPR_OK ? ok() : st;
 }
 
-upr_status upr_rank_candidates(const upr_model* m, const upr_kv_cache* cache,
-                               const upr_segments* hist, const void* cand_emb,
-                               const upr_segments* cand, float* scores, void* ws,
-                               size_t ws_bytes, void* stream) {
+// upr_rank_candidates, and with `scratch` its no-alloc variant, whose
+// workspace is the library's per-GPU scratch array (upr_noalloc.hip).
+static upr_status rank_entry(const upr_model* m, const upr_kv_cache* cache,
+                             const upr_segments* hist, const void* cand_emb,
+                             const upr_segments* cand, float* scores, void* ws,
+                             size_t ws_bytes, bool scratch, void* stream) {
     if (!m) return fail(UPR_ERR_NULL, "model is NULL");
     int64_t hf, hl, cf, cl;
     upr_status st = check_segments(hist, "hist", &hf, &hl);
@@ -875,6 +877,16 @@ upr_status upr_rank_candidates(const upr_model* m, const upr_kv_cache* cache,
         if (hl > hf && !cache->data) return fail(UPR_ERR_NULL, "cache data is NULL");
     }
     const upr::RankPlan p = upr::plan_rank(m->cfg, cand->num_users, cand->offsets_host);
+    if (scratch) {
+        if (p.bytes > UPR_NOALLOC_SCRATCH_BYTES)
+            return fail(UPR_ERR_LIMIT, "the call needs a %zu-byte workspace; the no-alloc scratch "
+                        "array holds %zu", p.bytes, (size_t)UPR_NOALLOC_SCRATCH_BYTES);
+        if (p.rows == 0) return ok();
+        const hipError_t e = upr::noalloc_scratch(&ws);
+        if (e != hipSuccess)
+            return fail(UPR_ERR_HIP, "scratch array lookup failed: %s", hipGetErrorString(e));
+        ws_bytes = UPR_NOALLOC_SCRATCH_BYTES;
+    }
     st = check_workspace(ws, ws_bytes, p.bytes);
     if (st != UPR_OK) return st;
     if (p.rows == 0) return ok();
@@ -890,6 +902,19 @@ upr_status upr_rank_candidates(const upr_model* m, const upr_kv_cache* cache,
              : upr::run_rank<upr::F32Types>(m, cache, hist, static_cast<const float*>(cand_emb),
                                             cand, out, p, w, s);
     return st == UPR_OK ? ok() : st;
+}
+
+upr_status upr_rank_candidates(const upr_model* m, const upr_kv_cache* cache,
+                               const upr_segments* hist, const void* cand_emb,
+                               const upr_segments* cand, float* scores, void* ws,
+                               size_t ws_bytes, void* stream) {
+    return rank_entry(m, cache, hist, cand_emb, cand, scores, ws, ws_bytes, false, stream);
+}
+
+upr_status upr_rank_candidates_noalloc(const upr_model* m, const upr_kv_cache* cache,
+                                       const upr_segments* hist, const void* cand_emb,
+                                       const upr_segments* cand, float* scores, void* stream) {
+    return rank_entry(m, cache, hist, cand_emb, cand, scores, nullptr, 0, true, stream);
 }
 
 // ---- per-action heads and utility top-K

@@ -189,4 +189,9 @@ hipError_t launch_attn_encode_simple(const TKV* q, TA* o, int64_t rows, int64_t 
                                      const TKV* cache_k, const TKV* cache_v, int64_t cache_cap,
                                      hipStream_t s);
 
+// Device address, on the current device, of the library's scratch array
+// for upr_rank_candidates_noalloc (UPR_NOALLOC_SCRATCH_BYTES, 256-byte
+// aligned; looked up once per device).
+hipError_t noalloc_scratch(void** ptr);
+
 }  // namespace upr

@@ -26,7 +26,8 @@ UPR_MX_IN_F32, UPR_MX_IN_F16, UPR_MX_IN_BF16 = 0, 1, 2
 EXPORTS = (
     "upr_weights_count", "upr_model_create", "upr_model_destroy", "upr_kv_cache_bytes",
     "upr_kv_cache_index", "upr_encode_workspace_bytes", "upr_rank_workspace_bytes",
-    "upr_encode_user", "upr_rank_candidates", "upr_status_string", "upr_last_error",
+    "upr_encode_user", "upr_rank_candidates", "upr_rank_candidates_noalloc",
+    "upr_status_string", "upr_last_error",
     "upr_profile_enable", "upr_profile_read",
     "upr_heads_weights_count", "upr_heads_create", "upr_heads_destroy",
     "upr_rank_actions_workspace_bytes", "upr_rank_actions", "upr_topk_by_utility",
@@ -88,6 +89,7 @@ def load(path: str = LIB_PATH):
         "upr_rank_workspace_bytes": (SZ, [VP, segp, segp]),
         "upr_encode_user": (I32, [VP, VP, segp, cachep, VP, SZ, VP]),
         "upr_rank_candidates": (I32, [VP, cachep, segp, VP, segp, VP, VP, SZ, VP]),
+        "upr_rank_candidates_noalloc": (I32, [VP, cachep, segp, VP, segp, VP, VP]),
         "upr_status_string": (ctypes.c_char_p, [I32]),
         "upr_last_error": (ctypes.c_char_p, []),
         "upr_profile_enable": (I32, [I32]),
@@ -173,6 +175,15 @@ def upr_rank_candidates(model, cache: upr_kv_cache, hist: upr_segments, cand_emb
                         cand: upr_segments, scores_ptr, ws_ptr, ws_bytes, stream) -> None:
     _check(load().upr_rank_candidates(model, ctypes.byref(cache), ctypes.byref(hist), cand_emb_ptr,
                                       ctypes.byref(cand), scores_ptr, ws_ptr, ws_bytes, stream))
+
+
+UPR_NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def upr_rank_candidates_noalloc(model, cache: upr_kv_cache, hist: upr_segments, cand_emb_ptr,
+                                cand: upr_segments, scores_ptr, stream) -> None:
+    _check(load().upr_rank_candidates_noalloc(model, ctypes.byref(cache), ctypes.byref(hist),
+                                              cand_emb_ptr, ctypes.byref(cand), scores_ptr, stream))
 
 
 def upr_heads_weights_count(cfg: upr_config, hc: upr_heads_config) -> int:

@@ -52,6 +52,8 @@ def kernel_work(inp):
         "rank.gemm_o": ("mfma", 2.0 * R * d * d),
         "rank.gemm_up": ("mfma", 2.0 * R * F * d),
         "rank.gemm_down": ("mfma", 2.0 * R * d * F),
+        # FFN up and down in one launch (hidden rows kept on chip)
+        "rank.ffn": ("mfma", 4.0 * R * d * F),
         # q.k and p.v over the history plus the candidate's own key
         "rank.attn": ("mfma", 4.0 * d * attn_pairs),
         # read the fp32 residual, write the normalised row
@@ -68,7 +70,7 @@ def kernel_work(inp):
 # two rocprofv3 --pmc passes scaled by a plain-copy calibration).  A record
 # only applies while its kernel source is unchanged.
 TRAFFIC_KEYS = {"rank.attn": "attn", "rank.gemm_qkv": "gemm_qkv", "rank.gemm_up": "gemm_up",
-                "rank.gemm_o": "gemm_o", "rank.gemm_down": "gemm_down"}
+                "rank.gemm_o": "gemm_o", "rank.gemm_down": "gemm_down", "rank.ffn": "ffn"}
 
 
 def measured_traffic(kernel, workload):

@@ -135,7 +135,9 @@ struct ImageBuilder {
     std::vector<char> img;
     upr_dtype dtype;
     static size_t align(size_t x) { return (x + 255) & ~size_t(255); }
-    size_t add_mat(const float* src, int64_t n, float* scale) {
+    // perm_row > 0: the matrix has rows of perm_row values whose columns are
+    // stored in the EPI_GELU_PERM order within each 16-column group.
+    size_t add_mat(const float* src, int64_t n, float* scale, int64_t perm_row = 0) {
         const bool bf = bf16_family(dtype);
         const size_t es = bf ? 2 : 4;
         size_t off = align(img.size());
@@ -154,12 +156,34 @@ struct ImageBuilder {
             const float up = std::ldexp(1.0f, k);
             *scale = std::ldexp(1.0f, -k);
             _Float16* dst = reinterpret_cast<_Float16*>(img.data() + off);
-            for (int64_t i = 0; i < n; ++i)
-                dst[i] = (_Float16)(bf16_value(f32_to_bf16_rne(src[i])) * up);
+            for (int64_t i = 0; i < n; ++i) {
+                const int64_t j = perm_row > 0 ? i - i % 16 + upr::kHidPerm[i % 16] : i;
+                dst[i] = (_Float16)(bf16_value(f32_to_bf16_rne(src[j])) * up);
+            }
         } else {
             std::memcpy(img.data() + off, src, n * 4);
         }
         return off;
+    }
+    // Fragment-major copy, for the fused FFN, of the fp16 matrix at `off`
+    // ([N, K] row-major, N a multiple of 32, K of 16): fragment (t, kk) is
+    // 64 lanes x 8 values, lane l taking row 32t + l % 32 at K positions
+    // 16kk + 8(l / 32) + e, e = 0..7 (the MFMA operand layout).
+    size_t add_frag(size_t off, int64_t N, int64_t K) {
+        const size_t dst_off = align(img.size());
+        img.resize(dst_off + N * K * 2);
+        const _Float16* src = reinterpret_cast<const _Float16*>(img.data() + off);
+        _Float16* dst = reinterpret_cast<_Float16*>(img.data() + dst_off);
+        const int64_t ksteps = K / 16;
+        for (int64_t t = 0; t < N / 32; ++t)
+            for (int64_t kk = 0; kk < ksteps; ++kk)
+                for (int l = 0; l < 64; ++l)
+                    for (int e = 0; e < 8; ++e) {
+                        const int64_t row = 32 * t + l % 32;
+                        const int64_t k = 16 * kk + 8 * (l / 32) + e;
+                        dst[((t * ksteps + kk) * 64 + l) * 8 + e] = src[row * K + k];
+                    }
+        return dst_off;
     }
     size_t add_vec(const float* src, int64_t n) {
         size_t off = align(img.size());
@@ -400,7 +424,7 @@ static bool fused_layernorm(const upr_config& c) {
 // head, scores[m] = LN_f(g[m]) . w + b with score_fin, and g is left stale.
 // Timing scopes are named "<stage>.gemm_o" etc.
 template <typename Types>
-static hipError_t launch_ffn_block(const char* const names[4], const upr_config& c,
+static hipError_t launch_ffn_block(const char* const names[5], const upr_config& c,
                                    const LayerWeights& w, const typename Types::act* o,
                                    typename Types::act* a, typename Types::act* h, float* g,
                                    int64_t R, const float* next_g, const float* next_b,
@@ -434,8 +458,32 @@ static hipError_t launch_ffn_block(const char* const names[4], const upr_config&
         e = launch_layernorm<TA>(g, a, R, d, w.ln2_g, w.ln2_b, eps, s);
     }
     if (e != hipSuccess) return e;
+    // the fused FFN (hidden rows kept on chip) when it ends in a LayerNorm
+    // or the score head
+    if constexpr (std::is_same_v<Types, Bf16Types>) {
+        if (fuse && w.W1p != nullptr && (next_g != nullptr || scores != nullptr) &&
+            ffn_fused_rows(R)) {
+            r.mode = scores != nullptr ? EPI_RESID_SCORE : EPI_RESID_LN;
+            r.resid_src = nullptr;
+            r.acc_scale = w.s_2;
+            r.bias = w.b2;
+            if (scores != nullptr) {
+                r.ln_gain = score_fin->lnf_g;
+                r.ln_shift = score_fin->lnf_b;
+                r.score_w = score_fin->w_score;
+                r.score_b = score_fin->b_score;
+                r.score_out = scores;
+            } else {
+                r.ln_gain = next_g;
+                r.ln_shift = next_b;
+            }
+            ProfScope ps(names[4], s);
+            return launch_ffn_fused(a, static_cast<const f16*>(w.W1p), static_cast<const f16*>(w.W2p),
+                                    w.b1, w.s_1, R, d, F, r, s);
+        }
+    }
     Epilogue up{};
-    up.mode = EPI_GELU;
+    up.mode = w.w2_perm ? EPI_GELU_PERM : EPI_GELU;
     up.acc_scale = w.s_1;
     up.bias = w.b1;
     up.out = h;
@@ -463,10 +511,10 @@ static hipError_t launch_ffn_block(const char* const names[4], const upr_config&
     return launch_gemm<TA, T>(h, F, static_cast<const TA*>(w.W2), R, d, F, r, s);
 }
 
-static const char* const kEncodeFfnNames[4] = {"encode.gemm_o", "encode.ln2", "encode.gemm_up",
-                                               "encode.gemm_down"};
-static const char* const kRankFfnNames[4] = {"rank.gemm_o", "rank.ln2", "rank.gemm_up",
-                                             "rank.gemm_down"};
+static const char* const kEncodeFfnNames[5] = {"encode.gemm_o", "encode.ln2", "encode.gemm_up",
+                                               "encode.gemm_down", "encode.ffn"};
+static const char* const kRankFfnNames[5] = {"rank.gemm_o", "rank.ln2", "rank.gemm_up",
+                                             "rank.gemm_down", "rank.ffn"};
 
 template <typename Types>
 static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_emb,
@@ -686,6 +734,8 @@ upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
     auto add_vec = [&](const float* src, int64_t n) { return ib.add_vec(src, n); };
     struct LayerOff {
         size_t Wqkv, Wo, W1, W2, ln1_g, ln1_b, bqkv, bo, ln2_g, ln2_b, b1, b2;
+        size_t W1p = 0, W2p = 0;    // fragment-major copies for the fused FFN (0: none)
+        bool w2_perm = false;
         float s_qkv, s_o, s_1, s_2;
         size_t mx[8];       // fp8 variant: qkv, qkv scales, o, o scales, 1, 1 scales, 2, 2 scales
     };
@@ -716,7 +766,16 @@ upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
         lo[l].Wqkv = add_mat(tmp.data(), 3 * d * d, &lo[l].s_qkv);
         lo[l].Wo = add_mat(Wo, d * d, &lo[l].s_o);
         lo[l].W1 = add_mat(W1, F * d, &lo[l].s_1);
-        lo[l].W2 = add_mat(W2, d * F, &lo[l].s_2);
+        // Shapes the fused FFN takes: W2's columns in the EPI_GELU_PERM
+        // order (so the FFN-up GEMM writes the hidden values in that order,
+        // and the unfused pair multiplies exactly the pairs the fused kernel
+        // does), and fragment-major copies of W1 and of that W2.
+        lo[l].w2_perm = bf16_family(c.dtype) && upr::ffn_fused_supported((int)d, (int)F);
+        lo[l].W2 = ib.add_mat(W2, d * F, &lo[l].s_2, lo[l].w2_perm ? F : 0);
+        if (lo[l].w2_perm) {
+            lo[l].W1p = ib.add_frag(lo[l].W1, F, d);
+            lo[l].W2p = ib.add_frag(lo[l].W2, d, F);
+        }
         if (mx) {
             ib.add_mx(tmp.data(), 3 * d, (int)d, &lo[l].mx[0], &lo[l].mx[1]);
             ib.add_mx(Wo, d, (int)d, &lo[l].mx[2], &lo[l].mx[3]);
@@ -756,6 +815,9 @@ upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
         w.Wo = base + lo[l].Wo;
         w.W1 = base + lo[l].W1;
         w.W2 = base + lo[l].W2;
+        w.W1p = lo[l].W1p ? base + lo[l].W1p : nullptr;
+        w.W2p = lo[l].W2p ? base + lo[l].W2p : nullptr;
+        w.w2_perm = lo[l].w2_perm;
         w.s_qkv = lo[l].s_qkv;
         w.s_o = lo[l].s_o;
         w.s_1 = lo[l].s_1;

@@ -39,6 +39,14 @@ struct LayerWeights {
     const void* Wo;
     const void* W1;
     const void* W2;
+    // fused FFN (bf16 models, supported shapes): W1 and W2 again in the
+    // fragment-major layout of the fused kernel (same values and scales);
+    // null when not built
+    const void* W1p;
+    const void* W2p;
+    // W2's columns are stored in the EPI_GELU_PERM order (with W1p/W2p):
+    // the FFN-up GEMM must then write its GELU output in that order
+    bool w2_perm;
     float s_qkv, s_o, s_1, s_2;
     // fp8 projection variant: the same matrices as MXFP8 (E4M3 codes
     // [out, in], E8M0 scales [out, in / 32]); null for other models
@@ -91,7 +99,17 @@ enum EpiMode : int {
                           // score_out[m] = LN(resid[m, :]) . score_w + *score_b
                           // (ln_gain, ln_shift, ln_eps = LN_f); the updated
                           // residual itself is not stored; N <= 512
+    EPI_GELU_PERM = 8,    // EPI_GELU with the columns of each 16-column group
+                          // stored in the order 0-3, 8-11, 4-7, 12-15 (position
+                          // p holds column kHidPerm[p]): the order in which the
+                          // fused FFN feeds the hidden values to the FFN-down
+                          // MFMAs, which a W2 with the same column order then
+                          // matches product for product
 };
+
+// The column order of EPI_GELU_PERM within a 16-column group (its own
+// inverse).
+constexpr int kHidPerm[16] = {0, 1, 2, 3, 8, 9, 10, 11, 4, 5, 6, 7, 12, 13, 14, 15};
 
 // Widest row (N) the residual update with LayerNorm (EPI_RESID_LN) handles.
 constexpr int kResidLnMaxN = 512;

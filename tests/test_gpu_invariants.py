@@ -86,6 +86,34 @@ def test_tile_height_does_not_change_scores():
         assert np.array_equal(s[co[u]:co[u + 1]], batch[co[u]:co[u + 1]]), f"user {u}"
 
 
+def test_fused_ffn_matches_unfused_pair_bit_exactly():
+    """The headline workload (128,000 candidate rows, 65,536 history rows:
+    the fused FFN in rank and encode) against single-user calls (the unfused
+    FFN-up / FFN-down pair on short tiles): the hidden values are written in
+    the order the fused kernel feeds them to the FFN-down MFMAs and W2 is
+    stored in that order, so both paths multiply the same pairs in the same
+    order and the scores and caches agree bit for bit."""
+    import torch
+    inp = make_workload("u64_n1024_k2000", seed=6)
+    say(f"[gpu] fused vs unfused FFN: {int(inp.cand_offsets[-1])} candidate rows, then single users")
+    run = GpuRun(inp)
+    run.encode()
+    run.rank()
+    batch = run.scores_np().copy()
+    cache = run.cache.clone()
+    ho, co = inp.hist_offsets, inp.cand_offsets
+    for u in [0, 29, inp.U - 1]:
+        run.scores.fill_(float("nan"))
+        h1, c1 = np.array([ho[u], ho[u + 1]], np.int32), np.array([co[u], co[u + 1]], np.int32)
+        run.cache.zero_()
+        run.encode(hoff=h1)
+        rows = slice(int(ho[u]), int(ho[u + 1]))
+        assert torch.equal(run.cache[:, :, :, rows], cache[:, :, :, rows]), f"cache of user {u}"
+        run.rank(hoff=h1, coff=c1)
+        s = run.scores_np()
+        assert np.array_equal(s[co[u]:co[u + 1]], batch[co[u]:co[u + 1]]), f"scores of user {u}"
+
+
 def test_tile_height_does_not_change_scores_mxfp8():
     """The same for the MXFP8 projection variant on the headline workload
     (128,000 candidate rows: tall tiles in every projection, 64-row tiles for

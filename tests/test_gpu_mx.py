@@ -310,7 +310,8 @@ def test_mxfp8_stages_split_check(case, monkeypatch):
     need = upr.upr_rank_workspace_bytes(run.model.handle, upr.segments(run.hoff, hd),
                                         upr.segments(run.coff, cd))
     tile = 128 if H * sum(-(-k // 128) for k in kl) >= 512 else 64
-    lay = _ws_layout(R, d, F, H * sum(-(-k // tile) for k in kl))
+    items = H * sum(-(-k // tile) for k in kl) if mfma_attn else 0      # MFMA attention's work list
+    lay = _ws_layout(R, d, F, items)
     assert lay["bytes"] == need, "workspace layout of the test differs from the library's"
     ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
     seq = _mx_sequence(d, L, mfma_attn)
@@ -388,7 +389,9 @@ def test_mxfp8_stages_split_check(case, monkeypatch):
                     spread[rows, sl] = p[:, :-1] @ np.abs(Vh) + p[:, -1:] * np.abs(vs) + np.abs(oo)
             delta = 2.0 ** -8 * spread + 1e-6
             if mfma_attn:
-                _check_encoding(cur["a"], cur["a_s"], o, delta, f"L{layer} attention", 0.05)
+                # bf16 probabilities move o by up to ~2^-9 relative: a few
+                # percent of the codes sit within that of a rounding boundary
+                _check_encoding(cur["a"], cur["a_s"], o, delta, f"L{layer} attention", 0.10)
             else:
                 _check_linear(cur["o"], o, 1e-5 * spread + 1e-6, f"L{layer} attention (fp32)")
         elif stage == "quant_o":

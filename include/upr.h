@@ -208,6 +208,76 @@ upr_status upr_rank_candidates_noalloc(const upr_model* model, const upr_kv_cach
                                        const upr_segments* cand, float* scores, void* stream);
 
 /* ---------------------------------------------------------------------
+ * Cross-process KV-cache pool (paper Sec. 3, "KV-cache sharing across
+ * stages": retrieval and ranking run as separate processes; the retrieval
+ * process pre-allocates a GPU pool of per-layer K/V slots, exports IPC
+ * handles for it to a per-instance file, and the ranking process maps the
+ * same allocation and reads the K/V retrieval wrote; slots are reused
+ * round-robin).
+ * A pool is one device allocation of `slots` caches of capacity_rows rows
+ * each, slot-major: slot s is a complete upr_kv_cache (the layout above) at
+ * byte offset s * upr_kv_cache_bytes(cfg, capacity_rows), so encode writes
+ * a slot and rank reads it in place (no per-request copy).  The allocation
+ * is at most UPR_KV_POOL_MAX_BYTES (UPR_ERR_LIMIT otherwise).  The creating
+ * process owns the allocation; other processes open it from a handle and
+ * must close it before the owner destroys it.  Ordering between processes
+ * (encode finished before another process ranks from the slot) is the
+ * callers' business, e.g. the owner synchronises its stream before it
+ * hands a slot identifier on.
+ * --------------------------------------------------------------------- */
+typedef struct upr_kv_pool upr_kv_pool;     /* opaque */
+
+#define UPR_KV_POOL_MAX_BYTES (((size_t)2 << 30) - 1)
+#define UPR_KV_POOL_MAGIC 0x50525055u       /* "UPRP" */
+
+/* What another process needs to open a pool: plain bytes, fit for a file. */
+typedef struct {
+    uint32_t magic;             /* UPR_KV_POOL_MAGIC                        */
+    int32_t slots;
+    int64_t capacity_rows;      /* rows per slot                            */
+    uint64_t bytes;             /* size of the allocation                   */
+    upr_config cfg;             /* the model shape the slots are laid out for */
+    uint8_t ipc[64];            /* hipIpcMemHandle_t of the allocation      */
+} upr_kv_pool_handle;
+
+/* Allocate a pool of `slots` >= 1 caches (device memory, contents
+ * undefined) on the current device.  *out is set only on UPR_OK. */
+upr_status upr_kv_pool_create(const upr_config* cfg, int32_t slots, int64_t capacity_rows,
+                              upr_kv_pool** out);
+
+/* The pool's handle (host struct), for upr_kv_pool_open in another process. */
+upr_status upr_kv_pool_export(const upr_kv_pool* pool, upr_kv_pool_handle* out);
+
+/* The same handle written to the file `path` (created or replaced whole:
+ * written to a temporary name, then renamed). */
+upr_status upr_kv_pool_export_file(const upr_kv_pool* pool, const char* path);
+
+/* Map a pool exported by another process (UPR_ERR_CONFIG if the handle is
+ * malformed, UPR_ERR_HIP if the mapping fails).  *out is set only on
+ * UPR_OK. */
+upr_status upr_kv_pool_open(const upr_kv_pool_handle* handle, upr_kv_pool** out);
+
+/* upr_kv_pool_open from a handle file written by upr_kv_pool_export_file. */
+upr_status upr_kv_pool_open_file(const char* path, upr_kv_pool** out);
+
+/* The cache of slot `slot` (0 <= slot < slots): data points into the pool
+ * (valid until the pool is destroyed), capacity_rows as the pool's. */
+upr_status upr_kv_pool_slot(const upr_kv_pool* pool, int32_t slot, upr_kv_cache* out);
+
+/* Next slot of the round-robin order 0, 1, .., slots-1, 0, .. (per pool
+ * object, thread-safe); -1 for a NULL pool. */
+int32_t upr_kv_pool_next_slot(upr_kv_pool* pool);
+
+/* Shape of the pool: the config, slot count and rows per slot (any output
+ * pointer may be NULL). */
+upr_status upr_kv_pool_info(const upr_kv_pool* pool, upr_config* cfg, int32_t* slots,
+                            int64_t* capacity_rows);
+
+/* Unmap (opened pool) or free (created pool); NULL is ignored.  No call may
+ * be using the pool. */
+void upr_kv_pool_destroy(upr_kv_pool* pool);
+
+/* ---------------------------------------------------------------------
  * Per-action ranking heads and utility top-K (paper Sec. 3: the ranking
  * objective of Masked Action Modeling gives every action type c = 1..C its
  * own MLP head h_psi_c producing a scalar logit from the transformer's

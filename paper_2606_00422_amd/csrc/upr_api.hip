@@ -270,6 +270,20 @@ void* plane_ptr(const upr_config& c, const upr_kv_cache* cache, int layer, int k
 // ---------------------------------------------------------------------------
 namespace upr {
 
+upr_status report_error(upr_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+upr_status report_ok() { return ok(); }
+
+upr_status validate_config(const upr_config* c) { return check_config(c); }
+
 // ---- MXFP8 on the host
 
 // E4M3 code of s (finite): nearest value, ties to even (nearbyint in the

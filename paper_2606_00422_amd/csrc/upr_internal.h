@@ -207,6 +207,14 @@ hipError_t launch_attn_encode_simple(const TKV* q, TA* o, int64_t rows, int64_t 
                                      const TKV* cache_k, const TKV* cache_v, int64_t cache_cap,
                                      hipStream_t s);
 
+// Error reporting shared by the C-interface source files: records a
+// formatted message for upr_last_error() and returns st (report_ok clears
+// it and returns UPR_OK); validate_config checks a upr_config as every
+// entry point does.
+upr_status report_error(upr_status st, const char* fmt, ...);
+upr_status report_ok();
+upr_status validate_config(const upr_config* c);
+
 // Device address, on the current device, of the library's scratch array
 // for upr_rank_candidates_noalloc (UPR_NOALLOC_SCRATCH_BYTES, 256-byte
 // aligned; looked up once per device).

@@ -32,6 +32,9 @@ EXPORTS = (
     "upr_heads_weights_count", "upr_heads_create", "upr_heads_destroy",
     "upr_rank_actions_workspace_bytes", "upr_rank_actions", "upr_topk_by_utility",
     "upr_mx_quantize_host", "upr_mx_quantize", "upr_mx_linear",
+    "upr_kv_pool_create", "upr_kv_pool_export", "upr_kv_pool_export_file", "upr_kv_pool_open",
+    "upr_kv_pool_open_file", "upr_kv_pool_slot", "upr_kv_pool_next_slot", "upr_kv_pool_info",
+    "upr_kv_pool_destroy",
 )
 
 
@@ -52,6 +55,16 @@ class upr_kv_cache(ctypes.Structure):
 
 class upr_heads_config(ctypes.Structure):
     _fields_ = [("n_actions", ctypes.c_int32), ("hidden", ctypes.c_int32)]
+
+
+UPR_KV_POOL_MAGIC = 0x50525055
+UPR_KV_POOL_MAX_BYTES = (2 << 30) - 1
+
+
+class upr_kv_pool_handle(ctypes.Structure):
+    _fields_ = [("magic", ctypes.c_uint32), ("slots", ctypes.c_int32),
+                ("capacity_rows", ctypes.c_int64), ("bytes", ctypes.c_uint64),
+                ("cfg", upr_config), ("ipc", ctypes.c_uint8 * 64)]
 
 
 class upr_kernel_stat(ctypes.Structure):
@@ -103,6 +116,15 @@ def load(path: str = LIB_PATH):
         "upr_mx_quantize_host": (I32, [VP, I64, I32, VP, VP]),
         "upr_mx_quantize": (I32, [VP, I32, I64, I32, VP, VP, VP]),
         "upr_mx_linear": (I32, [VP, VP, VP, VP, VP, I64, I32, I32, VP, VP]),
+        "upr_kv_pool_create": (I32, [cfgp, I32, I64, P(VP)]),
+        "upr_kv_pool_export": (I32, [VP, P(upr_kv_pool_handle)]),
+        "upr_kv_pool_export_file": (I32, [VP, ctypes.c_char_p]),
+        "upr_kv_pool_open": (I32, [P(upr_kv_pool_handle), P(VP)]),
+        "upr_kv_pool_open_file": (I32, [ctypes.c_char_p, P(VP)]),
+        "upr_kv_pool_slot": (I32, [VP, I32, cachep]),
+        "upr_kv_pool_next_slot": (I32, [VP]),
+        "upr_kv_pool_info": (I32, [VP, cfgp, P(I32), P(I64)]),
+        "upr_kv_pool_destroy": (None, [VP]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -315,6 +337,59 @@ def upr_mx_linear(a_codes, a_scales, w_codes, w_scales, bias, out, stream=None):
     _check(load().upr_mx_linear(a_codes.data_ptr(), a_scales.data_ptr(), w_codes.data_ptr(),
                                 w_scales.data_ptr(), bias.data_ptr(), M, N, K, out.data_ptr(),
                                 current_stream() if stream is None else stream))
+
+
+class KvPool:
+    """A cross-process KV-cache pool (upr_kv_pool_*): created here (owner) or
+    opened from another process's handle file."""
+
+    def __init__(self, handle: int):
+        self.handle = handle
+
+    @classmethod
+    def create(cls, cfg: upr_config, slots: int, capacity_rows: int) -> "KvPool":
+        out = ctypes.c_void_p()
+        _check(load().upr_kv_pool_create(ctypes.byref(cfg), slots, capacity_rows, ctypes.byref(out)))
+        return cls(int(out.value))
+
+    @classmethod
+    def open_file(cls, path: str) -> "KvPool":
+        out = ctypes.c_void_p()
+        _check(load().upr_kv_pool_open_file(os.fsencode(path), ctypes.byref(out)))
+        return cls(int(out.value))
+
+    @classmethod
+    def open(cls, h: upr_kv_pool_handle) -> "KvPool":
+        out = ctypes.c_void_p()
+        _check(load().upr_kv_pool_open(ctypes.byref(h), ctypes.byref(out)))
+        return cls(int(out.value))
+
+    def export(self) -> upr_kv_pool_handle:
+        h = upr_kv_pool_handle()
+        _check(load().upr_kv_pool_export(self.handle, ctypes.byref(h)))
+        return h
+
+    def export_file(self, path: str) -> None:
+        _check(load().upr_kv_pool_export_file(self.handle, os.fsencode(path)))
+
+    def slot(self, i: int) -> upr_kv_cache:
+        c = upr_kv_cache()
+        _check(load().upr_kv_pool_slot(self.handle, i, ctypes.byref(c)))
+        return c
+
+    def next_slot(self) -> int:
+        return int(load().upr_kv_pool_next_slot(self.handle))
+
+    def info(self):
+        cfg, slots, rows = upr_config(), ctypes.c_int32(), ctypes.c_int64()
+        _check(load().upr_kv_pool_info(self.handle, ctypes.byref(cfg), ctypes.byref(slots),
+                                       ctypes.byref(rows)))
+        return cfg, int(slots.value), int(rows.value)
+
+    def close(self):
+        if self.handle:
+            load().upr_kv_pool_destroy(self.handle)
+            self.handle = 0
 
 
 def current_stream() -> int:

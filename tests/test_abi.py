@@ -129,3 +129,34 @@ def test_mx_calls_validate_before_any_launch():
     assert lib.upr_mx_linear(None, None, None, None, None, 4, 12, 128, None, None) == upr.UPR_ERR_LIMIT
     assert lib.upr_mx_linear(None, None, None, None, None, 4, 16, 128, None, None) == upr.UPR_ERR_NULL
     assert lib.upr_mx_linear(None, None, None, None, None, 0, 16, 128, None, None) == upr.UPR_OK
+
+
+def test_kv_pool_validation_before_any_hip_call(tmp_path):
+    """Pool calls that must fail before touching the GPU: bad shapes, sizes
+    beyond the documented limit, malformed handles and files, NULL pools."""
+    lib = upr.load()
+    cfg = upr.make_config(512, 8, 4, 2048, "bf16")
+    out = ctypes.c_void_p()
+    bad = upr.make_config(96, 3, 1, 256, "bf16")
+    assert lib.upr_kv_pool_create(ctypes.byref(bad), 2, 16, ctypes.byref(out)) == upr.UPR_ERR_CONFIG
+    assert lib.upr_kv_pool_create(ctypes.byref(cfg), 0, 16, ctypes.byref(out)) == upr.UPR_ERR_LIMIT
+    assert lib.upr_kv_pool_create(ctypes.byref(cfg), 2, 0, ctypes.byref(out)) == upr.UPR_ERR_LIMIT
+    # 4 layers x 2 x 8 heads x 64 x 2 bytes = 8 KiB per row: 2^18 rows is 2 GiB
+    assert lib.upr_kv_pool_create(ctypes.byref(cfg), 1, 1 << 18, ctypes.byref(out)) == upr.UPR_ERR_LIMIT
+    assert lib.upr_kv_pool_create(ctypes.byref(cfg), 3, 100_000, ctypes.byref(out)) == upr.UPR_ERR_LIMIT
+    assert out.value is None
+    h = upr.upr_kv_pool_handle()
+    h.magic, h.slots, h.capacity_rows, h.cfg = 0x1234, 1, 16, cfg
+    assert lib.upr_kv_pool_open(ctypes.byref(h), ctypes.byref(out)) == upr.UPR_ERR_CONFIG
+    h.magic, h.bytes = upr.UPR_KV_POOL_MAGIC, 12345              # size inconsistent with the shape
+    assert lib.upr_kv_pool_open(ctypes.byref(h), ctypes.byref(out)) == upr.UPR_ERR_CONFIG
+    assert lib.upr_kv_pool_open_file(os.fsencode(str(tmp_path / "missing")), ctypes.byref(out)) == upr.UPR_ERR_LIMIT
+    short = tmp_path / "short"
+    short.write_bytes(b"UPRP")
+    assert lib.upr_kv_pool_open_file(os.fsencode(str(short)), ctypes.byref(out)) == upr.UPR_ERR_CONFIG
+    assert out.value is None
+    assert lib.upr_kv_pool_next_slot(None) == -1
+    c = upr.upr_kv_cache()
+    assert lib.upr_kv_pool_slot(None, 0, ctypes.byref(c)) == upr.UPR_ERR_NULL
+    assert lib.upr_kv_pool_info(None, None, None, None) == upr.UPR_ERR_NULL
+    lib.upr_kv_pool_destroy(None)

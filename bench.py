@@ -67,29 +67,37 @@ def kernel_work(inp):
 
 
 # Counter-measured HBM traffic per launch (profiles/traffic.json, written from
-# two rocprofv3 --pmc passes scaled by a plain-copy calibration).  A record
-# only applies while its kernel source is unchanged.
-TRAFFIC_KEYS = {"rank.attn": "attn", "rank.gemm_qkv": "gemm_qkv", "rank.gemm_up": "gemm_up",
-                "rank.gemm_o": "gemm_o", "rank.gemm_down": "gemm_down", "rank.ffn": "ffn"}
+# two rocprofv3 --pmc passes per workload, scaled by a plain-copy
+# calibration).  A record only applies to its own workload and while every
+# source its kernel is built from is unchanged.
+TRAFFIC_KEYS = {"rank.attn": "attn", "rank.gemm_qkv": "gemm_qkv", "rank.gemm_o": "gemm_o",
+                "rank.ffn": "ffn"}
+
+
+def _traffic_record(kernel, workload):
+    import hashlib
+    try:
+        rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))[workload][TRAFFIC_KEYS[kernel]]
+        h = hashlib.sha1()
+        for src in rec["sources"]:
+            h.update(open(os.path.join(ROOT, src), "rb").read())
+    except (OSError, KeyError, ValueError, TypeError):
+        return None
+    return rec if h.hexdigest()[:12] == rec["source_sha1"] else None
 
 
 def measured_traffic(kernel, workload):
-    import hashlib
-    try:
-        rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))[TRAFFIC_KEYS[kernel]]
-        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
-    except (OSError, KeyError, ValueError):
-        return None
-    if hashlib.sha1(src).hexdigest()[:12] != rec["source_sha1"] or rec["workload"] != workload:
-        return None
-    return round(rec["hbm_read_bytes"] + rec["hbm_write_bytes"])
+    rec = _traffic_record(kernel, workload)
+    return None if rec is None else round(rec["hbm_read_bytes"] + rec["hbm_write_bytes"])
 
 
-def traffic_provenance(kernel):
-    rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))[TRAFFIC_KEYS[kernel]]
-    return (f"profiles/traffic.json: rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE passes over "
-            f"{rec['source']} (sha1 {rec['source_sha1']}), each scaled by the same counter's "
-            f"reading for a plain device copy; replayed here while that source is unchanged")
+def traffic_provenance(kernel, workload):
+    rec = _traffic_record(kernel, workload)
+    return (f"profiles/traffic.json[{workload}][{TRAFFIC_KEYS[kernel]}]: rocprofv3 --pmc FETCH_SIZE "
+            f"and WRITE_SIZE passes over {', '.join(rec['sources'])} (sha1 {rec['source_sha1']}), "
+            f"each scaled by the same counter's reading for a plain device copy "
+            f"(x{1 / rec['fetch_factor']:.3f} and x{1 / rec['write_factor']:.3f}); "
+            f"replayed while those sources are unchanged")
 
 
 def path_flops(inp):
@@ -284,7 +292,7 @@ def dominant_roofline(prof, work, workload):
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic}
     roof["work_per_launch"] = amount
     roof["avg_launch_ms"] = round(avg_s * 1e3, 5)
-    roof["traffic_from"] = (traffic_provenance(dom) if traffic is not None else
+    roof["traffic_from"] = (traffic_provenance(dom, workload) if traffic is not None else
                             "null: no counter record for this kernel source and workload")
     return roof
 

@@ -114,9 +114,11 @@ def masked_softmax_attention(q, k, v, allowed):
 
     q [nq, D], k and v [nk, D], allowed bool [nq, nk] (every row allows at
     least one key).  Disallowed logits are -inf; the row maximum is
-    subtracted before exponentiating.
+    subtracted before exponentiating.  No queries: no output rows.
     """
     D = q.shape[-1]
+    if q.shape[0] == 0:
+        return np.zeros((0, v.shape[-1]))
     s = (q @ k.T) / math.sqrt(D)
     s = np.where(allowed, s, -np.inf)
     m = s.max(axis=-1, keepdims=True)

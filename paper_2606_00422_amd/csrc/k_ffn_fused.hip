@@ -37,6 +37,8 @@
 //  * Two workgroup barriers per chunk: before the chunk buffer is
 //    overwritten (every wave has finished the previous down phase) and
 //    after it is written.
+//  * A wave raises its issue priority for each run of MFMAs, so the other
+//    wave on its SIMD fills the matrix core's gaps with its loads and GELU.
 #include "gemm_tile.h"
 
 namespace upr {
@@ -209,10 +211,12 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ A,
         for (int s = 0; s < kUpSteps; ++s) {
             if (up_on && s + 1 < kUpSteps) a_frags(s + 1, af[(s + 1) & 1]);
             if (up_on) {
+                __builtin_amdgcn_s_setprio(1);
 #pragma unroll
                 for (int i = 0; i < kUT; ++i)
                     hacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ring[s % kRing], af[s & 1][i],
                                                                      hacc[i], 0, 0, 0);
+                __builtin_amdgcn_s_setprio(0);
             }
             refill(c, s);
             __builtin_amdgcn_sched_barrier(0);
@@ -279,10 +283,12 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ A,
             if (dn_on && q + 2 < kHQ) hf[(q + 2) % 3] = h_frag(q + 2);
             const int s0 = kUpSteps + 2 * kkp;
             if (dn_on) {
+                __builtin_amdgcn_s_setprio(1);
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
                     acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ring[(s0 + j) % kRing],
                                                                        hf[q % 3], acc[j][i], 0, 0, 0);
+                __builtin_amdgcn_s_setprio(0);
             }
             if (i == TM - 1) {
                 refill(c, s0);

@@ -52,8 +52,9 @@ def kernel_work(inp):
         "rank.gemm_o": ("mfma", 2.0 * R * d * d),
         "rank.gemm_up": ("mfma", 2.0 * R * F * d),
         "rank.gemm_down": ("mfma", 2.0 * R * d * F),
-        # FFN up and down in one launch (hidden rows kept on chip)
-        "rank.ffn": ("mfma", 4.0 * R * d * F),
+        # the layer's tail in one launch: O projection (with its residual
+        # update and LN2), FFN up and down, the hidden rows kept on chip
+        "rank.oproj_ffn": ("mfma", 2.0 * R * d * d + 4.0 * R * d * F),
         # q.k and p.v over the history plus the candidate's own key
         "rank.attn": ("mfma", 4.0 * d * attn_pairs),
         # read the fp32 residual, write the normalised row
@@ -71,7 +72,7 @@ def kernel_work(inp):
 # calibration).  A record only applies to its own workload and while every
 # source its kernel is built from is unchanged.
 TRAFFIC_KEYS = {"rank.attn": "attn", "rank.gemm_qkv": "gemm_qkv", "rank.gemm_o": "gemm_o",
-                "rank.ffn": "ffn"}
+                "rank.oproj_ffn": "oproj_ffn"}
 
 
 def _traffic_record(kernel, workload):

@@ -1,32 +1,42 @@
-// Fused FFN on the matrix cores, for bf16 models with d <= 512:
+// The tail of a layer on the matrix cores, for bf16 models with d <= 512:
+//   g[m, :] += o[m, :] Wo^T + bo;   a[m, :] = LN2(g[m, :])
 //   g[m, :] += gelu(a[m, :] W1^T + b1) W2^T + b2
 // followed by the LayerNorm of the updated rows (the next layer's LN1, or
 // LN_f before the action heads) or by the score head, as the projection
-// GEMM's whole-row epilogues do.  The F-wide hidden row never leaves the
-// compute unit: the unfused pair (FFN up with a GELU epilogue, FFN down)
-// writes and re-reads R x F fp16 values through HBM per layer.
+// GEMM's whole-row epilogues do.  Neither LN2's output nor the F-wide hidden
+// row leaves the compute unit: the unfused sequence (O projection with a
+// residual+LN2 epilogue, FFN up with a GELU epilogue, FFN down) writes and
+// re-reads R x d + R x F fp16 values through HBM per layer.
 //
 // One workgroup = 128 rows (TM = 4 row tiles of 32) and the whole output
 // row; eight waves.  Calls whose 128-row tiles would leave compute units idle
-// run the unfused pair on short tiles instead (ffn_fused_rows), with the
+// run the unfused sequence on short tiles instead (ffn_fused_rows), with the
 // same results bit for bit: both feed the matrix cores the same products in
-// the same order.
-//  * The rows of `a` (the LN2 output) are loaded once into LDS and stay
-//    there (d/64 blocks of [rows x 64], the GEMM's swizzled 128-byte rows).
+// the same order and round the same sums in the same order.
+//  * The tile's rows of the attention output o are loaded into LDS (d/64
+//    blocks of [rows x 64], the GEMM's swizzled 128-byte rows).
+//  * O projection: the eight waves side by side along the output (64
+//    columns each, all rows) accumulate o Wo^T over K = d, transposed as in
+//    the GEMM (Wo rows are the MFMA's first operand).  Its epilogue works in
+//    the MFMA layout (no LDS staging: the resident rows' LDS is where LN2
+//    goes): each lane updates and stores its own residual values, sums them
+//    for the row statistics in the same association tree as the GEMM's
+//    staged epilogue, and writes LN2 of its columns as fp16 straight into
+//    the resident-row layout, where a then stays.  The row statistics meet
+//    in the chunk buffer's LDS, free until the first chunk.
 //  * The hidden dimension is walked in chunks of 128.  Up phase: waves in a
-//    2 (rows) x 4 (hidden columns) grid compute h = a W1c^T, 64 x 32 each,
-//    transposed as in the GEMM (W1 rows are the MFMA's first operand).  Bias
-//    and GELU are applied in registers and the fp16 values go to the chunk
-//    buffer in LDS.  Down phase: the eight waves side by side along the
-//    output (64 columns each, all rows) accumulate h W2c^T into the fp32
-//    tile that the epilogue consumes.
+//    2 (rows) x 4 (hidden columns) grid compute h = a W1c^T, 64 x 32 each.
+//    Bias and GELU are applied in registers and the fp16 values go to the
+//    chunk buffer in LDS.  Down phase: as the O projection, the eight waves
+//    accumulate h W2c^T into the fp32 tile that the final epilogue consumes.
 //  * Weights come straight from global memory (L2) into registers, in a
 //    fragment-major layout built at model creation: fragment (t, kk) of a
 //    [N, K] matrix is 1 KB, lane l holding row 32t + l % 32 and eight
 //    consecutive positions 16kk + 8(l / 32) .. + 7 of K.  Every weight load
-//    of a wave is one coalesced 1 KB block, issued 5-8 fragments ahead; each
-//    step's code is kept in program order (scheduling barriers) so that the
-//    loads stay ahead and the LDS reads one step ahead.
+//    of a wave is one coalesced 1 KB block, issued 5-8 fragments ahead in
+//    one stream (Wo, then per chunk W1 and W2); each step's code is kept in
+//    program order (scheduling barriers) so that the loads stay ahead and
+//    the LDS reads one step ahead.
 //  * The hidden index of W2 is stored permuted within each 16-group
 //    (kHidPerm: 0-3, 8-11, 4-7, 12-15) so that the up phase's accumulator
 //    registers are the down phase's operand chunks as they are: lane
@@ -68,13 +78,181 @@ constexpr int smem_bytes() {
     return main > kEpiBytes ? main : kEpiBytes;
 }
 
-// KB = d / 64 (K-blocks of the up phase), TM = row tiles of 32.
+// Epilogue of the O projection in the MFMA layout: lane (row 32i + l%32,
+// half h) of wave w holds columns 64w + 32j + 8q + 4h + (0..3) of that row
+// in acc[j][i][4q .. 4q+3].  Per 32-row pass: g = r + (acc * s + bo) stored
+// back to the residual, the row's mean and squared deviations over the
+// wave's 64 columns, exchanged through `lnx` at a workgroup barrier, then
+// LN2 as fp16 into the resident rows' LDS (K-block w, the swizzled 128-byte
+// rows).  Association: the staged epilogue sums each run of four columns,
+// (x + y) + (z + w), then pairs the runs 32 columns apart, then 16, then 8,
+// then 4 (the exchange over its 16 lanes); here the same pairs are in
+// registers (j, then q's high bit, then its low bit) and the last is the
+// lane pair (l, l + 32), so the sums, and everything after, are the same
+// bits.  Rows past M: the residual descriptor ends at row M (loads read
+// zeros, stores are dropped); their LN2 values are finite and never stored.
+template <int TM, int KB>
+__device__ __forceinline__ void oproj_epilogue(f32x16 (&acc)[kTN][TM], f16* const sA, float* const lnx,
+                                               int64_t m0, int64_t M, const Epilogue& epa, int wave,
+                                               int lane, bool cols_on) {
+    constexpr int kRows = 32 * TM, kD = 64 * KB;
+    const int lrow = lane & 31, lhalf = lane >> 5;
+    const float sc = epa.acc_scale;
+    const int64_t rows_valid = M - m0 < kRows ? M - m0 : kRows;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        epa.resid + m0 * kD, (short)0, (int)(rows_valid * kD * 4), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<unsigned short*>(static_cast<const unsigned short*>(epa.resid_src)) + m0 * kD, (short)0,
+        (int)(rows_valid * kD * 2), 0x00020000);
+    const bool from_src = epa.resid_src != nullptr;
+    const float cnt = cols_on ? 64.f : 0.f;
+    const int colw = 64 * wave + 4 * lhalf;
+    // residual values of pass i (lane's row 32i + l%32), loaded one pass
+    // ahead
+    auto load_r = [&](int i, float4 (&dst)[kTN][4]) __attribute__((always_inline)) {
+        const unsigned vrow = (unsigned)(i * 32 + lrow) * kD;
+#pragma unroll
+        for (int j = 0; j < kTN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const unsigned col = (unsigned)(colw + 32 * j + 8 * q);
+                if (!cols_on) {
+                    dst[j][q] = make_float4(0.f, 0.f, 0.f, 0.f);
+                } else if (from_src) {
+                    typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
+                    const u32x2 w = __builtin_bit_cast(
+                        u32x2, __builtin_amdgcn_raw_buffer_load_b64(rsrc, (vrow + col) * 2, 0, 0));
+                    dst[j][q] = make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
+                                            __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u));
+                } else {
+                    dst[j][q] = __builtin_bit_cast(
+                        float4, __builtin_amdgcn_raw_buffer_load_b128(rs, (vrow + col) * 4, 0, 0));
+                }
+            }
+    };
+    float4 rb[2][kTN][4];
+    load_r(0, rb[0]);
+    // every wave has read its last fragment of o: the resident rows' LDS
+    // can take LN2
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        const unsigned vrow = (unsigned)(i * 32 + lrow) * kD;
+        if (i + 1 < TM) load_r(i + 1, rb[(i + 1) & 1]);
+        float4 (&o)[kTN][4] = rb[i & 1];
+#pragma unroll
+        for (int j = 0; j < kTN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int col = colw + 32 * j + 8 * q;
+                const float4 r = o[j][q];
+                const float4 b = cols_on ? *reinterpret_cast<const float4*>(epa.bias + col)
+                                         : make_float4(0.f, 0.f, 0.f, 0.f);
+                const f32x16& a = acc[j][i];
+                o[j][q] = make_float4(r.x + fmaf(a[4 * q + 0], sc, b.x), r.y + fmaf(a[4 * q + 1], sc, b.y),
+                                      r.z + fmaf(a[4 * q + 2], sc, b.z), r.w + fmaf(a[4 * q + 3], sc, b.w));
+                if (cols_on)
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o[j][q]), rs,
+                                                           (vrow + col) * 4, 0, 0);
+            }
+        // the row's sum over the wave's columns, then its squared deviations
+        auto tree = [&](const float (&t)[kTN][4]) {
+            float u[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) u[q] = t[0][q] + t[1][q];
+            const float v0 = u[0] + u[2], v1 = u[1] + u[3];
+            const float w = v0 + v1;
+            return w + __shfl_xor(w, 32, 64);
+        };
+        float t[kTN][4];
+#pragma unroll
+        for (int j = 0; j < kTN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                t[j][q] = cols_on ? (o[j][q].x + o[j][q].y) + (o[j][q].z + o[j][q].w) : 0.f;
+        const float mrow = cnt > 0.f ? tree(t) / cnt : 0.f;
+#pragma unroll
+        for (int j = 0; j < kTN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                float sq = 0.f;
+                if (cols_on) {
+                    const float u0 = o[j][q].x - mrow, u1 = o[j][q].y - mrow, u2 = o[j][q].z - mrow,
+                                u3 = o[j][q].w - mrow;
+                    sq = fmaf(u0, u0, fmaf(u1, u1, fmaf(u2, u2, u3 * u3)));
+                }
+                t[j][q] = sq;
+            }
+        const float qrow = tree(t);
+        float2* const X = reinterpret_cast<float2*>(lnx) + (i & 1) * (32 * 8);
+        if (lhalf == 0) X[lrow * 8 + wave] = make_float2(mrow, qrow);
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        const float4* const xr = reinterpret_cast<const float4*>(X + lrow * 8);
+        float mean_w[8], m2_w[8];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const float4 v = xr[k];
+            mean_w[2 * k] = v.x; m2_w[2 * k] = v.y; mean_w[2 * k + 1] = v.z; m2_w[2 * k + 1] = v.w;
+        }
+        float n_w[8], tot = 0.f, sum = 0.f;
+#pragma unroll
+        for (int w = 0; w < 8; ++w) {
+            const int c = kD - w * 64;
+            n_w[w] = (float)(c < 0 ? 0 : c > 64 ? 64 : c);
+            tot += n_w[w];
+            sum = fmaf(n_w[w], mean_w[w], sum);
+        }
+        const float mu = sum / tot;
+        float M2 = 0.f;
+#pragma unroll
+        for (int w = 0; w < 8; ++w) {
+            const float dm = mean_w[w] - mu;
+            M2 += fmaf(n_w[w] * dm, dm, m2_w[w]);
+        }
+        const float rstd = 1.0f / sqrtf(M2 / tot + epa.ln_eps);
+        if (cols_on) {
+            char* const rowp = reinterpret_cast<char*>(sA + wave * kRows * 64) + (i * 32 + lrow) * 128;
+            const int key = (lrow >> 1) & 7;
+#pragma unroll
+            for (int j = 0; j < kTN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int col = colw + 32 * j + 8 * q;
+                    const float4 g = *reinterpret_cast<const float4*>(epa.ln_gain + col);
+                    const float4 b = *reinterpret_cast<const float4*>(epa.ln_shift + col);
+                    const float4 h = o[j][q];
+                    const unsigned lo = pack2<false>(fmaf((h.x - mu) * rstd, g.x, b.x),
+                                                     fmaf((h.y - mu) * rstd, g.y, b.y));
+                    const unsigned hi = pack2<false>(fmaf((h.z - mu) * rstd, g.z, b.z),
+                                                     fmaf((h.w - mu) * rstd, g.w, b.w));
+                    typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
+                    *reinterpret_cast<u32x2*>(rowp + (((4 * j + q) ^ key) << 4) + 8 * lhalf) = u32x2{lo, hi};
+                }
+        }
+    }
+    // LN2 is in LDS before the up phase reads it (the residual stores are
+    // waited for before the final epilogue reads those rows back)
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// KB = d / 64 (K-blocks of the up phase), TM = row tiles of 32.  O: the
+// attention output rows (fp16, [M, d]).
 template <int MODE, int TM, int KB>
-__global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ A,
+__global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
+                                                      const h8* __restrict__ WoP,
                                                       const h8* __restrict__ W1p,
                                                       const h8* __restrict__ W2p,
                                                       const float* __restrict__ b1, float s1,
-                                                      int64_t M, int F, Epilogue epi) {
+                                                      int64_t M, int F, Epilogue epa, Epilogue epi) {
     constexpr int kRows = 32 * TM;
     constexpr int kD = 64 * KB;
     constexpr int kUpSteps = 4 * KB;                   // 16-deep k-steps of the up phase
@@ -101,12 +279,12 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ A,
     // down-phase role: output columns 64 wave .. +63
     const bool dn_on = kD == kMaxD || wave * 64 < kD;
 
-    // ---- resident rows of a: direct loads into LDS, 8 rows x 128 bytes of
-    // one K-block per instruction; rows past M read as zeros.
+    // ---- the tile's rows of o: direct loads into LDS, 8 rows x 128 bytes
+    // of one K-block per instruction; rows past M read as zeros.
     {
         const int64_t rows = M - m0 < kRows ? M - m0 : kRows;
         const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<f16*>(A + m0 * kD), (short)0, (int)(rows * kD * 2), 0x00020000);
+            const_cast<f16*>(O + m0 * kD), (short)0, (int)(rows * kD * 2), 0x00020000);
         const int r8 = lane >> 3, slot = lane & 7;
 #pragma unroll
         for (int ins = 0; ins < (kRows / 8) * KB / 8; ++ins) {
@@ -143,10 +321,26 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ A,
         return __builtin_bit_cast(h8, v);
     };
     auto active = [&](int s) { return s < kUpSteps ? up_on : dn_on; };
+    // O projection: k-step kk, column tile j of the wave is stream
+    // step 2 kk + j < kOSteps, Wo fragment (2 wave + j, kk); those steps
+    // come before chunk 0's.  Slots count from the start of chunk 0, so a
+    // chunk-0 fragment prefetched during the O projection lands in the slot
+    // the chunk loop reads it from.
+    constexpr int kOK = 4 * KB;                        // k-steps of the O projection (d / 16)
+    constexpr int kOSteps = 2 * kOK;
+    static_assert(kOSteps >= kRing, "the O projection fills the ring");
+    auto slot_o = [](int s) { return ((s - kOSteps) % kRing + kRing) % kRing; };
+    const __amdgpu_buffer_rsrc_t rsWo = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<h8*>(WoP), (short)0, kD * kD * 2, 0x00020000);
+    auto load_o = [&](int s) __attribute__((always_inline)) -> h8 {
+        const int kk = s >> 1, j = s & 1;
+        return __builtin_bit_cast(h8, __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                                    rsWo, lane_off, ((2 * wave + j) * kOK + kk) * 1024, 0)));
+    };
     h8 ring[kRing];
 #pragma unroll
     for (int s = 0; s < kRing; ++s)
-        if (active(s)) ring[s] = load_frag(0, s);
+        if (dn_on) ring[slot_o(s)] = load_o(s);
 
     f32x16 acc[kTN][TM];
 #pragma unroll
@@ -195,6 +389,56 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ A,
         const char* base = reinterpret_cast<const char*>(sH + (kkp >> 2) * kRows * 64);
         return *reinterpret_cast<const h8*>(base + (i * 32 + lrow) * 128 + choff[kkp & 3]);
     };
+
+    {
+        // ---- O projection: acc = o Wo^T, the operand fragments of o
+        // rolling through three registers two row tiles ahead of their
+        // MFMAs, as in the down phase
+        constexpr int kOQ = kOK * TM;
+        auto o_frag = [&](int q) __attribute__((always_inline)) -> h8 {
+            const int kk = q / TM, i = q % TM;
+            const char* base = reinterpret_cast<const char*>(sA + (kk >> 2) * kRows * 64);
+            return *reinterpret_cast<const h8*>(base + (i * 32 + lrow) * 128 + choff[kk & 3]);
+        };
+        auto refill_o = [&](int s) __attribute__((always_inline)) {
+            const int sn = s + kRing;
+            if (sn < kOSteps) {
+                if (dn_on) ring[slot_o(s)] = load_o(sn);
+            } else if (active(sn - kOSteps)) {
+                ring[slot_o(s)] = load_frag(0, sn - kOSteps);
+            }
+        };
+        h8 of[3];
+        if (dn_on) {
+            of[0] = o_frag(0);
+            of[1] = o_frag(1);
+        }
+#pragma unroll
+        for (int q = 0; q < kOQ; ++q) {
+            const int kk = q / TM, i = q % TM;
+            if (dn_on && q + 2 < kOQ) of[(q + 2) % 3] = o_frag(q + 2);
+            if (dn_on) {
+                __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ring[slot_o(2 * kk + j)], of[q % 3],
+                                                                       acc[j][i], 0, 0, 0);
+                __builtin_amdgcn_s_setprio(0);
+            }
+            if (i == TM - 1) {
+                refill_o(2 * kk);
+                refill_o(2 * kk + 1);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        oproj_epilogue<TM, KB>(acc, sA, reinterpret_cast<float*>(sH), m0, M, epa, wave, lane, dn_on);
+#pragma unroll
+        for (int j = 0; j < kTN; ++j)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
+    }
 
     for (int c = 0; c < nch; ++c) {
         // ---- up phase: h[kUT tiles][32 hidden] = a W1c^T.  Each step's code
@@ -302,7 +546,9 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ A,
     // whole rows.  Its staging regions reuse the resident rows' LDS and, for
     // 32-row tiles, the chunk buffer as well: every wave must have finished
     // its last down phase first (waves without output columns get here
-    // early).
+    // early).  The wave's residual stores of the O projection's epilogue
+    // (the rows it reads back) have completed.
+    __builtin_amdgcn_s_waitcnt(0x0F70);      // vmcnt(0)
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
@@ -313,22 +559,23 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ A,
 }
 
 template <int MODE, int TM>
-hipError_t launch_kb(int KB, unsigned grid, const f16* A, const h8* W1p, const h8* W2p,
-                     const float* b1, float s1, int64_t M, int F, const Epilogue& epi, hipStream_t s) {
+hipError_t launch_kb(int KB, unsigned grid, const f16* O, const h8* WoP, const h8* W1p, const h8* W2p,
+                     const float* b1, float s1, int64_t M, int F, const Epilogue& epa, const Epilogue& epi,
+                     hipStream_t s) {
     switch (KB) {
-        case 2: k_ffn_fused<MODE, TM, 2><<<grid, 512, 0, s>>>(A, W1p, W2p, b1, s1, M, F, epi); break;
-        case 4: k_ffn_fused<MODE, TM, 4><<<grid, 512, 0, s>>>(A, W1p, W2p, b1, s1, M, F, epi); break;
-        case 6: k_ffn_fused<MODE, TM, 6><<<grid, 512, 0, s>>>(A, W1p, W2p, b1, s1, M, F, epi); break;
-        case 8: k_ffn_fused<MODE, TM, 8><<<grid, 512, 0, s>>>(A, W1p, W2p, b1, s1, M, F, epi); break;
+        case 2: k_ffn_fused<MODE, TM, 2><<<grid, 512, 0, s>>>(O, WoP, W1p, W2p, b1, s1, M, F, epa, epi); break;
+        case 4: k_ffn_fused<MODE, TM, 4><<<grid, 512, 0, s>>>(O, WoP, W1p, W2p, b1, s1, M, F, epa, epi); break;
+        case 6: k_ffn_fused<MODE, TM, 6><<<grid, 512, 0, s>>>(O, WoP, W1p, W2p, b1, s1, M, F, epa, epi); break;
+        case 8: k_ffn_fused<MODE, TM, 8><<<grid, 512, 0, s>>>(O, WoP, W1p, W2p, b1, s1, M, F, epa, epi); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 template <int MODE>
-hipError_t launch_mode(const f16* A, const h8* W1p, const h8* W2p, const float* b1, float s1,
-                       int64_t M, int d, int F, const Epilogue& epi, hipStream_t s) {
-    return launch_kb<MODE, 4>(d / 64, (unsigned)((M + 127) / 128), A, W1p, W2p, b1, s1, M, F, epi, s);
+hipError_t launch_mode(const f16* O, const h8* WoP, const Epilogue& epa, const h8* W1p, const h8* W2p,
+                       const float* b1, float s1, int64_t M, int d, int F, const Epilogue& epi, hipStream_t s) {
+    return launch_kb<MODE, 4>(d / 64, (unsigned)((M + 127) / 128), O, WoP, W1p, W2p, b1, s1, M, F, epa, epi, s);
 }
 
 }  // namespace ffn_detail
@@ -339,21 +586,26 @@ bool ffn_fused_supported(int d, int F) {
     return (d == 128 || d == 256 || d == 384 || d == 512) && F > 0 && F % ffn_detail::kFC == 0;
 }
 
-hipError_t launch_ffn_fused(const f16* A, const f16* W1p, const f16* W2p, const float* b1,
-                            float s1, int64_t M, int d, int F, const Epilogue& epi, hipStream_t s) {
+hipError_t launch_ffn_fused(const f16* O, const f16* WoP, const Epilogue& epa, const f16* W1p,
+                            const f16* W2p, const float* b1, float s1, int64_t M, int d, int F,
+                            const Epilogue& epi, hipStream_t s) {
     using namespace ffn_detail;
     if (M == 0) return hipSuccess;
     if (!ffn_fused_supported(d, F) || epi.ldr != d || !epi.ln_gain || !epi.ln_shift)
         return hipErrorInvalidValue;
+    if (epa.mode != EPI_RESID_LN || epa.resid != epi.resid || epa.ldr != d || !epa.bias || !epa.ln_gain ||
+        !epa.ln_shift)
+        return hipErrorInvalidValue;
+    const h8* wo = reinterpret_cast<const h8*>(WoP);
     const h8* w1 = reinterpret_cast<const h8*>(W1p);
     const h8* w2 = reinterpret_cast<const h8*>(W2p);
     switch (epi.mode) {
         case EPI_RESID_LN:
             if (!epi.ln_out || epi.ln_ldo % 4 != 0) return hipErrorInvalidValue;
-            return launch_mode<EPI_RESID_LN>(A, w1, w2, b1, s1, M, d, F, epi, s);
+            return launch_mode<EPI_RESID_LN>(O, wo, epa, w1, w2, b1, s1, M, d, F, epi, s);
         case EPI_RESID_SCORE:
             if (!epi.score_w || !epi.score_b || !epi.score_out) return hipErrorInvalidValue;
-            return launch_mode<EPI_RESID_SCORE>(A, w1, w2, b1, s1, M, d, F, epi, s);
+            return launch_mode<EPI_RESID_SCORE>(O, wo, epa, w1, w2, b1, s1, M, d, F, epi, s);
         default: return hipErrorInvalidValue;
     }
 }

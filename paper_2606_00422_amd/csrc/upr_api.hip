@@ -436,7 +436,8 @@ static bool fused_layernorm(const upr_config& c) {
 // written and the O projection reads the residual from these token rows.
 // scores (last ranking layer, fused LayerNorms): FFN down ends in the score
 // head, scores[m] = LN_f(g[m]) . w + b with score_fin, and g is left stale.
-// Timing scopes are named "<stage>.gemm_o" etc.
+// Timing scopes are named "<stage>.gemm_o" etc.; the one-kernel tail is
+// "<stage>.oproj_ffn".
 template <typename Types>
 static hipError_t launch_ffn_block(const char* const names[5], const upr_config& c,
                                    const LayerWeights& w, const typename Types::act* o,
@@ -449,7 +450,7 @@ static hipError_t launch_ffn_block(const char* const names[5], const upr_config&
     const int d = c.d_model, F = c.d_ff;
     const float eps = c.ln_eps;
     const bool fuse = fused_layernorm<Types>(c);
-    hipError_t e;
+    hipError_t e = hipSuccess;
     Epilogue r{};
     r.mode = fuse ? EPI_RESID_LN : EPI_RESID;
     r.acc_scale = w.s_o;
@@ -462,7 +463,12 @@ static hipError_t launch_ffn_block(const char* const names[5], const upr_config&
     r.ln_out = a;
     r.ln_ldo = d;
     r.resid_src = resid_src;
-    {
+    // the layer's tail in one kernel (O projection, residual update, LN2,
+    // FFN with its hidden rows on chip, then the next LayerNorm or the score
+    // head) for calls whose 128-row tiles fill the device
+    const bool tail = std::is_same_v<Types, Bf16Types> && fuse && w.WoP != nullptr && w.W1p != nullptr &&
+                      (next_g != nullptr || scores != nullptr) && ffn_fused_rows(R);
+    if (!tail) {
         ProfScope ps(names[0], s);
         e = launch_gemm<TA, T>(o, d, static_cast<const TA*>(w.Wo), R, d, d, r, s);
     }
@@ -472,11 +478,9 @@ static hipError_t launch_ffn_block(const char* const names[5], const upr_config&
         e = launch_layernorm<TA>(g, a, R, d, w.ln2_g, w.ln2_b, eps, s);
     }
     if (e != hipSuccess) return e;
-    // the fused FFN (hidden rows kept on chip) when it ends in a LayerNorm
-    // or the score head
     if constexpr (std::is_same_v<Types, Bf16Types>) {
-        if (fuse && w.W1p != nullptr && (next_g != nullptr || scores != nullptr) &&
-            ffn_fused_rows(R)) {
+        if (tail) {
+            const Epilogue oproj = r;
             r.mode = scores != nullptr ? EPI_RESID_SCORE : EPI_RESID_LN;
             r.resid_src = nullptr;
             r.acc_scale = w.s_2;
@@ -492,8 +496,9 @@ static hipError_t launch_ffn_block(const char* const names[5], const upr_config&
                 r.ln_shift = next_b;
             }
             ProfScope ps(names[4], s);
-            return launch_ffn_fused(a, static_cast<const f16*>(w.W1p), static_cast<const f16*>(w.W2p),
-                                    w.b1, w.s_1, R, d, F, r, s);
+            return launch_ffn_fused(reinterpret_cast<const f16*>(o), static_cast<const f16*>(w.WoP), oproj,
+                                    static_cast<const f16*>(w.W1p), static_cast<const f16*>(w.W2p), w.b1,
+                                    w.s_1, R, d, F, r, s);
         }
     }
     Epilogue up{};
@@ -526,9 +531,9 @@ static hipError_t launch_ffn_block(const char* const names[5], const upr_config&
 }
 
 static const char* const kEncodeFfnNames[5] = {"encode.gemm_o", "encode.ln2", "encode.gemm_up",
-                                               "encode.gemm_down", "encode.ffn"};
+                                               "encode.gemm_down", "encode.oproj_ffn"};
 static const char* const kRankFfnNames[5] = {"rank.gemm_o", "rank.ln2", "rank.gemm_up",
-                                             "rank.gemm_down", "rank.ffn"};
+                                             "rank.gemm_down", "rank.oproj_ffn"};
 
 template <typename Types>
 static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_emb,
@@ -748,7 +753,7 @@ upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
     auto add_vec = [&](const float* src, int64_t n) { return ib.add_vec(src, n); };
     struct LayerOff {
         size_t Wqkv, Wo, W1, W2, ln1_g, ln1_b, bqkv, bo, ln2_g, ln2_b, b1, b2;
-        size_t W1p = 0, W2p = 0;    // fragment-major copies for the fused FFN (0: none)
+        size_t WoP = 0, W1p = 0, W2p = 0;   // fragment-major copies for the fused FFN (0: none)
         bool w2_perm = false;
         float s_qkv, s_o, s_1, s_2;
         size_t mx[8];       // fp8 variant: qkv, qkv scales, o, o scales, 1, 1 scales, 2, 2 scales
@@ -787,6 +792,7 @@ upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
         lo[l].w2_perm = bf16_family(c.dtype) && upr::ffn_fused_supported((int)d, (int)F);
         lo[l].W2 = ib.add_mat(W2, d * F, &lo[l].s_2, lo[l].w2_perm ? F : 0);
         if (lo[l].w2_perm) {
+            lo[l].WoP = ib.add_frag(lo[l].Wo, d, d);
             lo[l].W1p = ib.add_frag(lo[l].W1, F, d);
             lo[l].W2p = ib.add_frag(lo[l].W2, d, F);
         }
@@ -829,6 +835,7 @@ upr_status upr_model_create(const upr_config* cfg, const float* weights_host,
         w.Wo = base + lo[l].Wo;
         w.W1 = base + lo[l].W1;
         w.W2 = base + lo[l].W2;
+        w.WoP = lo[l].WoP ? base + lo[l].WoP : nullptr;
         w.W1p = lo[l].W1p ? base + lo[l].W1p : nullptr;
         w.W2p = lo[l].W2p ? base + lo[l].W2p : nullptr;
         w.w2_perm = lo[l].w2_perm;

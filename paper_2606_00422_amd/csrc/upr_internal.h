@@ -39,9 +39,10 @@ struct LayerWeights {
     const void* Wo;
     const void* W1;
     const void* W2;
-    // fused FFN (bf16 models, supported shapes): W1 and W2 again in the
+    // fused FFN (bf16 models, supported shapes): Wo, W1 and W2 again in the
     // fragment-major layout of the fused kernel (same values and scales);
     // null when not built
+    const void* WoP;
     const void* W1p;
     const void* W2p;
     // W2's columns are stored in the EPI_GELU_PERM order (with W1p/W2p):

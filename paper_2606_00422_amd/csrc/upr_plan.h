@@ -123,18 +123,23 @@ hipError_t launch_gemm(const TA* A, int64_t lda, const TA* W, int64_t M, int N, 
 hipError_t launch_gemm_mfma(const f16* A, int64_t lda, const f16* W, int64_t M, int N, int K,
                             const Epilogue& epi, hipStream_t s);
 
-// Fused FFN (k_ffn_fused.hip): g += gelu(A W1^T + b1) W2^T + b2 on the
-// fp32 residual (epi.resid, epi.acc_scale = W2's scale, epi.bias = b2),
-// then the LayerNorm (EPI_RESID_LN) or the score head (EPI_RESID_SCORE).
-// A [M, d] fp16 rows (leading dimension d); W1p [F, d] and W2p [d, F] in
-// the fragment-major layout of pack_ffn_weight; s1 = W1's scale.
+// Fused layer tail (k_ffn_fused.hip) on the fp32 residual g:
+//   g += O Wo^T + bo;  a = LN2(g);  g += gelu(a W1^T + b1) W2^T + b2
+// then the LayerNorm (epi.mode EPI_RESID_LN) or the score head
+// (EPI_RESID_SCORE).  O [M, d] fp16 attention output rows (leading dimension
+// d); epa: the O projection's EPI_RESID_LN epilogue (Wo's scale, bo, LN2,
+// the same residual; resid_src in the first layer), epi: the FFN down's
+// (W2's scale, b2, the following LayerNorm or score head).  WoP [d, d],
+// W1p [F, d] and W2p [d, F] in the fragment-major layout the model image
+// builds; s1 = W1's scale.
 bool ffn_fused_supported(int d, int F);
 // Whether a call of M rows takes the fused kernel: its 128-row tiles must
-// fill the device.  Smaller calls run the unfused pair on short tiles, with
-// bit-identical results (same products in the same order).
+// fill the device.  Smaller calls run the unfused sequence on short tiles,
+// with bit-identical results (same products in the same order).
 bool ffn_fused_rows(int64_t M);
-hipError_t launch_ffn_fused(const f16* A, const f16* W1p, const f16* W2p, const float* b1,
-                            float s1, int64_t M, int d, int F, const Epilogue& epi, hipStream_t s);
+hipError_t launch_ffn_fused(const f16* O, const f16* WoP, const Epilogue& epa, const f16* W1p,
+                            const f16* W2p, const float* b1, float s1, int64_t M, int d, int F,
+                            const Epilogue& epi, hipStream_t s);
 
 // Work list of the MFMA attention: entries (user, head, first query row,
 // query count) over the rows of `row_offsets` (candidates, or the history

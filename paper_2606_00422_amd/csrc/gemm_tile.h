@@ -146,7 +146,9 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
             const_cast<unsigned short*>(static_cast<const unsigned short*>(epi.resid_src)) + wrow0 * epi.ldr,
             (short)0, (int)(rows_valid * epi.ldr * 2), 0x00020000);
         const bool from_src = epi.resid_src != nullptr;
+        const bool acc_has_resid = (MODE == EPI_RESID_LN || MODE == EPI_RESID_SCORE) && epi.acc_resid != 0;
         auto load_resid = [&](int i, float4 (&dst)[8]) {
+            if (acc_has_resid) return;          // the accumulators carry it
             if (from_src) {
                 typedef __attribute__((ext_vector_type(2))) unsigned u32x2;
 #pragma unroll
@@ -363,8 +365,11 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
             for (int p = 0; p < 8; ++p) {
                 const float4 r = g[i & 1][p];
                 const u32x4 o = __builtin_bit_cast(
-                    u32x4, make_float4(r.x + fmaf(x[p].x, sc, bias4.x), r.y + fmaf(x[p].y, sc, bias4.y),
-                                       r.z + fmaf(x[p].z, sc, bias4.z), r.w + fmaf(x[p].w, sc, bias4.w)));
+                    u32x4, acc_has_resid
+                               ? make_float4(fmaf(x[p].x, sc, bias4.x), fmaf(x[p].y, sc, bias4.y),
+                                             fmaf(x[p].z, sc, bias4.z), fmaf(x[p].w, sc, bias4.w))
+                               : make_float4(r.x + fmaf(x[p].x, sc, bias4.x), r.y + fmaf(x[p].y, sc, bias4.y),
+                                             r.z + fmaf(x[p].z, sc, bias4.z), r.w + fmaf(x[p].w, sc, bias4.w)));
                 if constexpr (!kScore)
                     __builtin_amdgcn_raw_buffer_store_b128(o, rs, vo + (unsigned)(i * 32 + p * 4) * ldr4, 0,
                                                            2 /* nt */);
@@ -546,6 +551,37 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kTN][kTM], char* 
             __builtin_amdgcn_wave_barrier();
         }
     }
+}
+
+// Accumulators of a wave's tile set to resid / acc_scale (Epilogue::
+// acc_resid): register r of tile (j, i) takes row wrow0 + 32i + lane%32,
+// column wcol0 + 32j + 8(r/4) + 4(lane/32) + r%4, one float4 per run of four
+// columns; rows past M read zeros (buffer range), columns past N stay zero.
+template <int kTM>
+__device__ __forceinline__ void load_acc_resid(f32x16 (&acc)[kTN][kTM], const Epilogue& epi, int64_t wrow0,
+                                               int wcol0, int64_t M, int N, int lane) {
+    constexpr int kWM = 32 * kTM;
+    const int lrow = lane & 31, lhalf = lane >> 5;
+    const float inv = 1.0f / epi.acc_scale;     // a power of two: exact
+    const int64_t rows_valid = M - wrow0 < 0 ? 0 : (M - wrow0 < kWM ? M - wrow0 : kWM);
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        epi.resid + wrow0 * epi.ldr, (short)0, (int)(rows_valid * epi.ldr * 4), 0x00020000);
+#pragma unroll
+    for (int j = 0; j < kTN; ++j)
+#pragma unroll
+        for (int i = 0; i < kTM; ++i)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int col = wcol0 + 32 * j + 8 * q + 4 * lhalf;
+                float4 r = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (col < N)                           // N is a multiple of 8
+                    r = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                       rs, (unsigned)((i * 32 + lrow) * epi.ldr + col) * 4u, 0, 0));
+                acc[j][i][4 * q + 0] = r.x * inv;
+                acc[j][i][4 * q + 1] = r.y * inv;
+                acc[j][i][4 * q + 2] = r.z * inv;
+                acc[j][i][4 * q + 3] = r.w * inv;
+            }
 }
 
 // Compute units of the current device.

@@ -19,11 +19,13 @@
 //    columns each, all rows) accumulate o Wo^T over K = d, transposed as in
 //    the GEMM (Wo rows are the MFMA's first operand).  Its epilogue works in
 //    the MFMA layout (no LDS staging: the resident rows' LDS is where LN2
-//    goes): each lane updates and stores its own residual values, sums them
-//    for the row statistics in the same association tree as the GEMM's
-//    staged epilogue, and writes LN2 of its columns as fp16 straight into
-//    the resident-row layout, where a then stays.  The row statistics meet
-//    in the chunk buffer's LDS, free until the first chunk.
+//    goes): each lane updates its own residual values, sums them for the
+//    row statistics in the same association tree as the GEMM's staged
+//    epilogue, and writes LN2 of its columns as fp16 straight into the
+//    resident-row layout, where a then stays.  The row statistics meet in
+//    the chunk buffer's LDS, free until the first chunk.  The updated
+//    residual never goes to HBM: it stays in the accumulators, divided by
+//    W2's power-of-two scale, as the FFN down's starting value.
 //  * The hidden dimension is walked in chunks of 128.  Up phase: waves in a
 //    2 (rows) x 4 (hidden columns) grid compute h = a W1c^T, 64 x 32 each.
 //    Bias and GELU are applied in registers and the fp16 values go to the
@@ -80,21 +82,24 @@ constexpr int smem_bytes() {
 
 // Epilogue of the O projection in the MFMA layout: lane (row 32i + l%32,
 // half h) of wave w holds columns 64w + 32j + 8q + 4h + (0..3) of that row
-// in acc[j][i][4q .. 4q+3].  Per 32-row pass: g = r + (acc * s + bo) stored
-// back to the residual, the row's mean and squared deviations over the
-// wave's 64 columns, exchanged through `lnx` at a workgroup barrier, then
-// LN2 as fp16 into the resident rows' LDS (K-block w, the swizzled 128-byte
-// rows).  Association: the staged epilogue sums each run of four columns,
+// in acc[j][i][4q .. 4q+3].  Per 32-row pass: g = r + (acc * s + bo), the
+// row's mean and squared deviations over the wave's 64 columns, exchanged
+// through `lnx` at a workgroup barrier, then LN2 as fp16 into the resident
+// rows' LDS (K-block w, the swizzled 128-byte rows).  g itself is not
+// stored: acc[j][i] leaves as g * inv2 (inv2 = 1 / FFN down's scale, a power
+// of two), the starting value of the FFN down accumulators, so the final
+// epilogue's update acc * s2 + b2 completes the residual stream (as the
+// unfused FFN-down GEMM does when it loads g into its accumulators).  Association: the staged epilogue sums each run of four columns,
 // (x + y) + (z + w), then pairs the runs 32 columns apart, then 16, then 8,
 // then 4 (the exchange over its 16 lanes); here the same pairs are in
 // registers (j, then q's high bit, then its low bit) and the last is the
 // lane pair (l, l + 32), so the sums, and everything after, are the same
 // bits.  Rows past M: the residual descriptor ends at row M (loads read
-// zeros, stores are dropped); their LN2 values are finite and never stored.
+// zeros); their values are finite and never stored.
 template <int TM, int KB>
 __device__ __forceinline__ void oproj_epilogue(f32x16 (&acc)[kTN][TM], f16* const sA, float* const lnx,
-                                               int64_t m0, int64_t M, const Epilogue& epa, int wave,
-                                               int lane, bool cols_on) {
+                                               int64_t m0, int64_t M, const Epilogue& epa, float inv2,
+                                               int wave, int lane, bool cols_on) {
     constexpr int kRows = 32 * TM, kD = 64 * KB;
     const int lrow = lane & 31, lhalf = lane >> 5;
     const float sc = epa.acc_scale;
@@ -107,8 +112,8 @@ __device__ __forceinline__ void oproj_epilogue(f32x16 (&acc)[kTN][TM], f16* cons
     const bool from_src = epa.resid_src != nullptr;
     const float cnt = cols_on ? 64.f : 0.f;
     const int colw = 64 * wave + 4 * lhalf;
-    // residual values of pass i (lane's row 32i + l%32), loaded one pass
-    // ahead
+    // residual values of pass i (lane's row 32i + l%32); the first pass's
+    // are requested before the barrier
     auto load_r = [&](int i, float4 (&dst)[kTN][4]) __attribute__((always_inline)) {
         const unsigned vrow = (unsigned)(i * 32 + lrow) * kD;
 #pragma unroll
@@ -130,8 +135,8 @@ __device__ __forceinline__ void oproj_epilogue(f32x16 (&acc)[kTN][TM], f16* cons
                 }
             }
     };
-    float4 rb[2][kTN][4];
-    load_r(0, rb[0]);
+    float4 rb[kTN][4];
+    load_r(0, rb);
     // every wave has read its last fragment of o: the resident rows' LDS
     // can take LN2
     __builtin_amdgcn_s_waitcnt(0xC07F);
@@ -140,9 +145,8 @@ __device__ __forceinline__ void oproj_epilogue(f32x16 (&acc)[kTN][TM], f16* cons
     asm volatile("" ::: "memory");
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
-        const unsigned vrow = (unsigned)(i * 32 + lrow) * kD;
-        if (i + 1 < TM) load_r(i + 1, rb[(i + 1) & 1]);
-        float4 (&o)[kTN][4] = rb[i & 1];
+        if (i > 0) load_r(i, rb);
+        float4 (&o)[kTN][4] = rb;
 #pragma unroll
         for (int j = 0; j < kTN; ++j)
 #pragma unroll
@@ -151,12 +155,13 @@ __device__ __forceinline__ void oproj_epilogue(f32x16 (&acc)[kTN][TM], f16* cons
                 const float4 r = o[j][q];
                 const float4 b = cols_on ? *reinterpret_cast<const float4*>(epa.bias + col)
                                          : make_float4(0.f, 0.f, 0.f, 0.f);
-                const f32x16& a = acc[j][i];
+                f32x16& a = acc[j][i];
                 o[j][q] = make_float4(r.x + fmaf(a[4 * q + 0], sc, b.x), r.y + fmaf(a[4 * q + 1], sc, b.y),
                                       r.z + fmaf(a[4 * q + 2], sc, b.z), r.w + fmaf(a[4 * q + 3], sc, b.w));
-                if (cols_on)
-                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o[j][q]), rs,
-                                                           (vrow + col) * 4, 0, 0);
+                a[4 * q + 0] = o[j][q].x * inv2;
+                a[4 * q + 1] = o[j][q].y * inv2;
+                a[4 * q + 2] = o[j][q].z * inv2;
+                a[4 * q + 3] = o[j][q].w * inv2;
             }
         // the row's sum over the wave's columns, then its squared deviations
         auto tree = [&](const float (&t)[kTN][4]) {
@@ -236,8 +241,7 @@ __device__ __forceinline__ void oproj_epilogue(f32x16 (&acc)[kTN][TM], f16* cons
                 }
         }
     }
-    // LN2 is in LDS before the up phase reads it (the residual stores are
-    // waited for before the final epilogue reads those rows back)
+    // LN2 is in LDS before the up phase reads it
     __builtin_amdgcn_s_waitcnt(0xC07F);
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
@@ -431,13 +435,9 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        oproj_epilogue<TM, KB>(acc, sA, reinterpret_cast<float*>(sH), m0, M, epa, wave, lane, dn_on);
-#pragma unroll
-        for (int j = 0; j < kTN; ++j)
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
+        // (acc leaves holding the updated residual / FFN down's scale)
+        oproj_epilogue<TM, KB>(acc, sA, reinterpret_cast<float*>(sH), m0, M, epa, 1.0f / epi.acc_scale,
+                               wave, lane, dn_on);
     }
 
     for (int c = 0; c < nch; ++c) {
@@ -546,9 +546,7 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
     // whole rows.  Its staging regions reuse the resident rows' LDS and, for
     // 32-row tiles, the chunk buffer as well: every wave must have finished
     // its last down phase first (waves without output columns get here
-    // early).  The wave's residual stores of the O projection's epilogue
-    // (the rows it reads back) have completed.
-    __builtin_amdgcn_s_waitcnt(0x0F70);      // vmcnt(0)
+    // early).
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
@@ -593,8 +591,8 @@ hipError_t launch_ffn_fused(const f16* O, const f16* WoP, const Epilogue& epa, c
     if (M == 0) return hipSuccess;
     if (!ffn_fused_supported(d, F) || epi.ldr != d || !epi.ln_gain || !epi.ln_shift)
         return hipErrorInvalidValue;
-    if (epa.mode != EPI_RESID_LN || epa.resid != epi.resid || epa.ldr != d || !epa.bias || !epa.ln_gain ||
-        !epa.ln_shift)
+    if (epa.mode != EPI_RESID_LN || epa.acc_resid || epa.resid != epi.resid || epa.ldr != d || !epa.bias ||
+        !epa.ln_gain || !epa.ln_shift || !epi.acc_resid)
         return hipErrorInvalidValue;
     const h8* wo = reinterpret_cast<const h8*>(WoP);
     const h8* w1 = reinterpret_cast<const h8*>(W1p);

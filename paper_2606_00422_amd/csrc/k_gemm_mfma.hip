@@ -187,6 +187,9 @@ __global__ __launch_bounds__(kThreads, 1) void k_gemm_mfma(const void* __restric
         for (int i = 0; i < kTM; ++i)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
+    // (FFN down with its LayerNorm: the accumulators start at the residual)
+    if constexpr (!MX && (MODE == EPI_RESID_LN || MODE == EPI_RESID_SCORE))
+        if (epi.acc_resid) load_acc_resid<kTM>(acc, epi, m0 + wm * kWM, n0 + wn * kWN, M, N, lane);
 
     const int lrow = lane & 31, lhalf = lane >> 5;
     // fp16: 16-deep fragments; MXFP8: 64-deep fragments + scale dwords.  Each

@@ -483,6 +483,7 @@ static hipError_t launch_ffn_block(const char* const names[5], const upr_config&
             const Epilogue oproj = r;
             r.mode = scores != nullptr ? EPI_RESID_SCORE : EPI_RESID_LN;
             r.resid_src = nullptr;
+            r.acc_resid = 1;
             r.acc_scale = w.s_2;
             r.bias = w.b2;
             if (scores != nullptr) {
@@ -526,6 +527,9 @@ static hipError_t launch_ffn_block(const char* const names[5], const upr_config&
     r.bias = w.b2;
     r.ln_gain = next_g;
     r.ln_shift = next_b;
+    // FFN down with its LayerNorm or score head accumulates onto the
+    // residual (the fused tail's arithmetic, so both give the same bits)
+    r.acc_resid = std::is_same_v<Types, Bf16Types> && (r.mode == EPI_RESID_LN || r.mode == EPI_RESID_SCORE);
     ProfScope ps(names[3], s);
     return launch_gemm<TA, T>(h, F, static_cast<const TA*>(w.W2), R, d, F, r, s);
 }

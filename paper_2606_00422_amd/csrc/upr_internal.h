@@ -145,6 +145,12 @@ struct Epilogue {
     // (leading dimension ldr) instead of resid, and the sum still goes to
     // resid: the first layer's update reads the tokens themselves
     const void* resid_src;
+    // EPI_RESID_LN / EPI_RESID_SCORE with fp16 operands: nonzero when the
+    // accumulators start at resid / acc_scale instead of zero (acc_scale a
+    // power of two, so the division is exact).  The update is then
+    // acc * acc_scale + bias, with no residual read in the epilogue: the FFN
+    // down accumulates onto the residual that the O projection produced.
+    int acc_resid;
     // EPI_RESID_SCORE
     const float* score_w;   // [N]
     const float* score_b;   // one value

@@ -9,8 +9,8 @@
 // included): for history position i,  o_i = softmax([q_i . K_t]_t<=i) V.
 // Queries are pre-scaled by log2(e)/sqrt(D), so the softmax uses exp2.
 //
-// One workgroup = one work item (user, head, up to 128 candidates or 256
-// history rows); four waves of 32 (ranking) or 64 (encode) queries.  The
+// One workgroup = one work item (user, head, up to 128 candidates or 128
+// history rows); four waves of 32 queries.  The
 // user's cached K/V for this layer and head are
 // streamed through LDS in 64-key stages (double-buffered, loaded straight
 // from global memory into LDS) and shared by all queries of the item.  Per
@@ -56,9 +56,10 @@ constexpr int kKS = 64;           // keys per LDS stage
 // 16-query groups per wave: ranking 2 (128 VGPRs, four waves per SIMD: the
 // latency of one wave's exponentials and LDS reads hides behind three
 // others), or 1 for calls too small to fill the device with 128-candidate
-// items (each query's arithmetic is the same either way); the causal pass 4
-// (fewer K/V reads per query; its diagonal sub-blocks are masked per wave)
-constexpr int kRankQG = 2, kSmallRankQG = 1, kEncodeQG = 4;
+// items (each query's arithmetic is the same either way); the causal pass
+// 2 as well (four waves per SIMD; 64 queries per wave, at two waves per
+// SIMD, read half the K/V per query but measured 21% slower)
+constexpr int kRankQG = 2, kSmallRankQG = 1, kEncodeQG = 2;
 static_assert(4 * 16 * kRankQG == kRankAttnTile, "ranking work-list tile must match the kernel");
 static_assert(4 * 16 * kSmallRankQG == kSmallRankAttnTile, "small-call tile must match the kernel");
 static_assert(4 * 16 * kEncodeQG == kAttnTile, "encode work-list tile must match the kernel");

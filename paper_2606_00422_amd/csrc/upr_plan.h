@@ -14,7 +14,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 // Query rows per work item of the MFMA attention (one workgroup handles this
 // many history rows, in the causal encode pass, or candidates, in ranking,
 // of one user for one head).
-constexpr int kAttnTile = 256;
+constexpr int kAttnTile = 128;
 constexpr int kRankAttnTile = 128;
 constexpr int kSmallRankAttnTile = 64;      // ranking calls with few work items
 constexpr int64_t kSmallRankItems = 512;    // fewer 128-candidate items than this

@@ -58,7 +58,7 @@ constexpr int kKS = 64;           // keys per LDS stage
 // others), or 1 for calls too small to fill the device with 128-candidate
 // items (each query's arithmetic is the same either way); the causal pass
 // 2 as well (four waves per SIMD; 64 queries per wave, at two waves per
-// SIMD, read half the K/V per query but measured 21% slower)
+// SIMD, read half the K/V per query but measured 26% slower)
 constexpr int kRankQG = 2, kSmallRankQG = 1, kEncodeQG = 2;
 static_assert(4 * 16 * kRankQG == kRankAttnTile, "ranking work-list tile must match the kernel");
 static_assert(4 * 16 * kSmallRankQG == kSmallRankAttnTile, "small-call tile must match the kernel");

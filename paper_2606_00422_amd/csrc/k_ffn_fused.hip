@@ -98,8 +98,9 @@ constexpr int smem_bytes() {
 // zeros); their values are finite and never stored.
 template <int TM, int KB>
 __device__ __forceinline__ void oproj_epilogue(f32x16 (&acc)[kTN][TM], f16* const sA, float* const lnx,
-                                               int64_t m0, int64_t M, const Epilogue& epa, float inv2,
-                                               int wave, int lane, bool cols_on) {
+                                               const float* const par, int64_t m0, int64_t M,
+                                               const Epilogue& epa, float inv2, int wave, int lane,
+                                               bool cols_on) {
     constexpr int kRows = 32 * TM, kD = 64 * KB;
     const int lrow = lane & 31, lhalf = lane >> 5;
     const float sc = epa.acc_scale;
@@ -153,7 +154,7 @@ __device__ __forceinline__ void oproj_epilogue(f32x16 (&acc)[kTN][TM], f16* cons
             for (int q = 0; q < 4; ++q) {
                 const int col = colw + 32 * j + 8 * q;
                 const float4 r = o[j][q];
-                const float4 b = cols_on ? *reinterpret_cast<const float4*>(epa.bias + col)
+                const float4 b = cols_on ? *reinterpret_cast<const float4*>(par + col)
                                          : make_float4(0.f, 0.f, 0.f, 0.f);
                 f32x16& a = acc[j][i];
                 o[j][q] = make_float4(r.x + fmaf(a[4 * q + 0], sc, b.x), r.y + fmaf(a[4 * q + 1], sc, b.y),
@@ -229,8 +230,8 @@ __device__ __forceinline__ void oproj_epilogue(f32x16 (&acc)[kTN][TM], f16* cons
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const int col = colw + 32 * j + 8 * q;
-                    const float4 g = *reinterpret_cast<const float4*>(epa.ln_gain + col);
-                    const float4 b = *reinterpret_cast<const float4*>(epa.ln_shift + col);
+                    const float4 g = *reinterpret_cast<const float4*>(par + kD + col);
+                    const float4 b = *reinterpret_cast<const float4*>(par + 2 * kD + col);
                     const float4 h = o[j][q];
                     const unsigned lo = pack2<false>(fmaf((h.x - mu) * rstd, g.x, b.x),
                                                      fmaf((h.y - mu) * rstd, g.y, b.y));
@@ -267,6 +268,13 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
     __shared__ __attribute__((aligned(16))) char smem[smem_bytes<TM>()];
     f16* const sA = reinterpret_cast<f16*>(smem);                          // [KB][kRows x 64]
     f16* const sH = reinterpret_cast<f16*>(smem + kRows * kMaxD * 2);      // [2][kRows x 64]
+    // The O projection epilogue's bias, LN2 gain and LN2 shift ([3][kD]),
+    // staged once behind its statistics exchange in the chunk buffer's LDS
+    // (free until the first chunk), so that its passes read them from LDS
+    // instead of one global round trip per column group and pass.
+    constexpr int kLnxBytes = 2 * 32 * 8 * 8;
+    static_assert(kLnxBytes + 3 * kMaxD * 4 <= 32 * TM * kFC * 2, "parameters fit in the chunk buffer");
+    float* const sPar = reinterpret_cast<float*>(smem + kRows * kMaxD * 2 + kLnxBytes);
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -283,6 +291,12 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
     // down-phase role: output columns 64 wave .. +63
     const bool dn_on = kD == kMaxD || wave * 64 < kD;
 
+    float par[3];
+    if (tid < kD) {
+        par[0] = epa.bias[tid];
+        par[1] = epa.ln_gain[tid];
+        par[2] = epa.ln_shift[tid];
+    }
     // ---- the tile's rows of o: direct loads into LDS, 8 rows x 128 bytes
     // of one K-block per instruction; rows past M read as zeros.
     {
@@ -355,6 +369,11 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
             for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
 
     __builtin_amdgcn_s_waitcnt(0x0F70);      // vmcnt(0): the resident rows have landed
+    if (tid < kD) {
+        sPar[tid] = par[0];
+        sPar[kD + tid] = par[1];
+        sPar[2 * kD + tid] = par[2];
+    }
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
@@ -436,7 +455,7 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
             __builtin_amdgcn_sched_barrier(0);
         }
         // (acc leaves holding the updated residual / FFN down's scale)
-        oproj_epilogue<TM, KB>(acc, sA, reinterpret_cast<float*>(sH), m0, M, epa, 1.0f / epi.acc_scale,
+        oproj_epilogue<TM, KB>(acc, sA, reinterpret_cast<float*>(sH), sPar, m0, M, epa, 1.0f / epi.acc_scale,
                                wave, lane, dn_on);
     }
 

@@ -75,9 +75,11 @@ constexpr int kMaxLayers = 64;
 // fp16/bf16 conversion in code whose unrolled copies serve different rows:
 // without it the compiler may fold the producing multiply into a
 // mixed-precision instruction (one rounding) in some copies and not in others
-// (two roundings), so a row's result would depend on its position.
+// (two roundings), so a row's result would depend on its position.  Not
+// volatile: a volatile statement would also fence the scheduler, keeping
+// loads behind it from being issued early.
 __device__ __forceinline__ float keep_f32(float x) {
-    asm volatile("" : "+v"(x));
+    asm("" : "+v"(x));
     return x;
 }
 

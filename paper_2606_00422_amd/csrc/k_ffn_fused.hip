@@ -36,9 +36,10 @@
 //    [N, K] matrix is 1 KB, lane l holding row 32t + l % 32 and eight
 //    consecutive positions 16kk + 8(l / 32) .. + 7 of K.  Every weight load
 //    of a wave is one coalesced 1 KB block, issued 5-8 fragments ahead in
-//    one stream (Wo, then per chunk W1 and W2); each step's code is kept in
-//    program order (scheduling barriers) so that the loads stay ahead and
-//    the LDS reads one step ahead.
+//    one stream (Wo, W1 of chunk 0, then W1 of chunk c with W2 of chunk
+//    c - 1); each step's code is kept in program order (scheduling
+//    barriers) so that the loads stay ahead and the LDS reads one step
+//    ahead.
 //  * The hidden index of W2 is stored permuted within each 16-group
 //    (kHidPerm: 0-3, 8-11, 4-7, 12-15) so that the up phase's accumulator
 //    registers are the down phase's operand chunks as they are: lane
@@ -46,9 +47,14 @@
 //    (q, s = 0..3), i.e. positions 8h .. 8h + 7 of the permuted order of the
 //    16-groups {q = 0, 1} and {q = 2, 3}.  Each lane writes two 16-byte
 //    chunks per row tile, no shuffles.
-//  * Two workgroup barriers per chunk: before the chunk buffer is
-//    overwritten (every wave has finished the previous down phase) and
-//    after it is written.
+//  * Each wave runs the up phase and GELU of chunk c before the down phase
+//    of chunk c - 1 (whose hidden values are in the chunk buffer), then two
+//    workgroup barriers: before the buffer is overwritten with chunk c
+//    (every wave has finished the down phase) and after it is written.
+//    With no barrier between a wave's GELU and its next MFMAs, the two
+//    waves of a SIMD drift apart and one's GELU overlaps the other's
+//    matrix-core work (1-1.5% faster than the down phase right after the
+//    write, bit-identical).
 //  * A wave raises its issue priority for each run of MFMAs, so the other
 //    wave on its SIMD fills the matrix core's gaps with its loads and GELU.
 #include "gemm_tile.h"
@@ -326,19 +332,16 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
     const __amdgpu_buffer_rsrc_t rsW2 = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<h8*>(W2p), (short)0, (int)((int64_t)F * kD * 2), 0x00020000);
     const int lane_off = lane * 16;
-    auto load_frag = [&](int c, int s) __attribute__((always_inline)) -> h8 {
-        u32x4 v;
-        if (s < kUpSteps) {
-            v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                              rsW1, lane_off, ((4 * c + un) * kUpSteps + s) * 1024, 0));
-        } else {
-            const int q = s - kUpSteps, kkp = q >> 1, j = q & 1;
-            v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                              rsW2, lane_off, ((2 * wave + j) * fsteps + 8 * c + kkp) * 1024, 0));
-        }
-        return __builtin_bit_cast(h8, v);
+    auto load_w1 = [&](int c, int s) __attribute__((always_inline)) -> u32x4 {
+        return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                          rsW1, lane_off, ((4 * c + un) * kUpSteps + s) * 1024, 0));
     };
-    auto active = [&](int s) { return s < kUpSteps ? up_on : dn_on; };
+    auto load_w2 = [&](int c, int q) __attribute__((always_inline)) -> u32x4 {
+        const int kkp = q >> 1, j = q & 1;
+        return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                          rsW2, lane_off, ((2 * wave + j) * fsteps + 8 * c + kkp) * 1024, 0));
+    };
+    constexpr int kW2Steps = 2 * kDownSteps;
     // O projection: k-step kk, column tile j of the wave is stream
     // step 2 kk + j < kOSteps, Wo fragment (2 wave + j, kk); those steps
     // come before chunk 0's.  Slots count from the start of chunk 0, so a
@@ -350,12 +353,12 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
     auto slot_o = [](int s) { return ((s - kOSteps) % kRing + kRing) % kRing; };
     const __amdgpu_buffer_rsrc_t rsWo = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<h8*>(WoP), (short)0, kD * kD * 2, 0x00020000);
-    auto load_o = [&](int s) __attribute__((always_inline)) -> h8 {
+    auto load_o = [&](int s) __attribute__((always_inline)) -> u32x4 {
         const int kk = s >> 1, j = s & 1;
-        return __builtin_bit_cast(h8, __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                                    rsWo, lane_off, ((2 * wave + j) * kOK + kk) * 1024, 0)));
+        return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                                    rsWo, lane_off, ((2 * wave + j) * kOK + kk) * 1024, 0));
     };
-    h8 ring[kRing];
+    u32x4 ring[kRing];     // fragments as 32-bit words (16-bit vector phis get split)
 #pragma unroll
     for (int s = 0; s < kRing; ++s)
         if (dn_on) ring[slot_o(s)] = load_o(s);
@@ -385,20 +388,6 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
 #pragma unroll
     for (int m = 0; m < 4; ++m) choff[m] = (((2 * m + lhalf) ^ ((lrow >> 1) & 7)) << 4);
 
-    // One weight-stream step: fragment s of chunk c is consumed, and the slot
-    // refilled with the fragment kRing steps later (this chunk's or the
-    // next one's).
-    // (After the last chunk the prefetch still runs: W1 fragments of chunk
-    // nch lie past the end of W1p and read as zeros, W2 fragments of chunk
-    // nch are the next tile's first ones; either way nothing uses them.)
-    auto refill = [&](int c, int s) __attribute__((always_inline)) {
-        const int sn = s + kRing;
-        if (sn < kSteps) {
-            if (active(sn)) ring[s % kRing] = load_frag(c, sn);
-        } else if (active(sn - kSteps)) {
-            ring[s % kRing] = load_frag(c + 1, sn - kSteps);
-        }
-    };
     // operand fragments from LDS, read one step ahead of their MFMAs
     auto a_frags = [&](int s, h8 (&dst)[kUT]) __attribute__((always_inline)) {
         const char* base = reinterpret_cast<const char*>(sA + (s >> 2) * kRows * 64);
@@ -427,8 +416,8 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
             const int sn = s + kRing;
             if (sn < kOSteps) {
                 if (dn_on) ring[slot_o(s)] = load_o(sn);
-            } else if (active(sn - kOSteps)) {
-                ring[slot_o(s)] = load_frag(0, sn - kOSteps);
+            } else if (up_on) {
+                ring[slot_o(s)] = load_w1(0, sn - kOSteps);
             }
         };
         h8 of[3];
@@ -444,7 +433,7 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
                 __builtin_amdgcn_s_setprio(1);
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
-                    acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ring[slot_o(2 * kk + j)], of[q % 3],
+                    acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8, ring[slot_o(2 * kk + j)]), of[q % 3],
                                                                        acc[j][i], 0, 0, 0);
                 __builtin_amdgcn_s_setprio(0);
             }
@@ -459,10 +448,61 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
                                wave, lane, dn_on);
     }
 
-    for (int c = 0; c < nch; ++c) {
-        // ---- up phase: h[kUT tiles][32 hidden] = a W1c^T.  Each step's code
-        // stays in program order (scheduling barriers), so the weight loads
-        // remain kRing steps ahead of their use and the LDS reads one step.
+
+    // ---- the weight stream after the O projection, in blocks: block 0 is
+    // chunk 0's W1 steps; block c (1 <= c < nch) holds chunk c's W1 steps,
+    // then chunk c - 1's W2 steps; the last block is the last chunk's W2
+    // steps.  Blocks after the first are kSteps long, a multiple of kRing,
+    // so a step's slot follows from its place in its block alone; a consumed
+    // slot is refilled with the step kRing later.  Where the next step may
+    // lie in either matrix (at a block boundary) the choice is made on the
+    // scalar unit, so the ring slots need no branch merges.  Loads past a
+    // matrix's end read zeros (W1 past the last chunk; W2 rows of waves
+    // without output columns) and are never used.
+    auto load_sel = [&](bool w1, int c1, int s1, int c2, int q2) __attribute__((always_inline)) -> u32x4 {
+        const int o1 = ((4 * c1 + un) * kUpSteps + s1) * 1024;
+        const int o2 = ((2 * wave + (q2 & 1)) * fsteps + 8 * c2 + (q2 >> 1)) * 1024;
+        return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(w1 ? rsW1 : rsW2, lane_off,
+                                                                               w1 ? o1 : o2, 0));
+    };
+    // step sp of block c (1 <= c <= nch; block nch is the last one)
+    auto fetch = [&](int c, int sp) __attribute__((always_inline)) -> u32x4 {
+        // (a step across a block boundary has sp < kRing <= 2 kDownSteps,
+        // which in the last block is a W2 step)
+        if (sp < kUpSteps) return load_sel(c < nch, c, sp, c - 1, sp);
+        return load_w2(c - 1, sp - kUpSteps);
+    };
+    auto refill_first = [&](int s) __attribute__((always_inline)) {           // block 0
+        const int sn = s + kRing;
+        ring[s % kRing] = sn < kUpSteps ? load_w1(0, sn) : fetch(1, sn - kUpSteps);
+    };
+    auto refill_mid = [&](int c, int s) __attribute__((always_inline)) {      // block c
+        const int sn = s + kRing;
+        ring[(kUpSteps + s) % kRing] = sn < kSteps ? fetch(c, sn) : fetch(c + 1, sn - kSteps);
+    };
+    auto refill_last = [&](int j) __attribute__((always_inline)) {          // last block
+        const int jn = j + kRing;
+        ring[(kUpSteps + j) % kRing] = jn < kW2Steps ? load_w2(nch - 1, jn) : load_w1(nch, jn - kW2Steps);
+    };
+
+    // The lane's LDS offsets pass through an opaque statement at the start
+    // of each phase, so the compiler derives the phase's fragment addresses
+    // there instead of keeping every one of them live across the chunk loop.
+    auto fresh_offsets = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int m = 0; m < 4; ++m) asm volatile("" : "+v"(choff[m]));
+    };
+    // ---- up phase: h[kUT tiles][32 hidden] = a W1c^T, its weight steps at
+    // slots (base + s) % kRing; then bias, GELU and fp16 into pk.  Each
+    // step's code stays in program order (scheduling barriers), so the
+    // weight loads remain kRing steps ahead of their use and the LDS reads
+    // one step.  The chunk's bias is requested with the first step, ahead
+    // of the ring loads that GELU must not wait for.
+    unsigned pk[kUT][2][4];
+    auto up_gelu = [&](auto base_c, int c, auto&& refill) __attribute__((always_inline)) {
+        constexpr int base = decltype(base_c)::value;
+        fresh_offsets();
+        float4 bq[4];
         f32x16 hacc[kUT];
 #pragma unroll
         for (int i = 0; i < kUT; ++i)
@@ -477,27 +517,24 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
                 __builtin_amdgcn_s_setprio(1);
 #pragma unroll
                 for (int i = 0; i < kUT; ++i)
-                    hacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ring[s % kRing], af[s & 1][i],
+                    hacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8, ring[(base + s) % kRing]), af[s & 1][i],
                                                                      hacc[i], 0, 0, 0);
                 __builtin_amdgcn_s_setprio(0);
             }
-            refill(c, s);
+            refill(s);
             __builtin_amdgcn_sched_barrier(0);
         }
-        // ---- bias, GELU, fp16: lane (row, half h) holds hidden columns
-        // 32 un + 8q + 4h + s of its rows; chunk b of a row tile takes q in
-        // {2b, 2b + 1}, i.e. down-phase k-step 2 un + b, half h.
-        u32x4 hv[kUT][2];
+        // lane (row, half h) holds hidden columns 32 un + 8q + 4h + s of its
+        // rows; chunk b of a row tile takes q in {2b, 2b + 1}, i.e.
+        // down-phase k-step 2 un + b, half h
         if (up_on) {
-            float4 bq[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q)
                 bq[q] = *reinterpret_cast<const float4*>(b1 + c * kFC + 32 * un + 8 * q + 4 * lhalf);
 #pragma unroll
             for (int i = 0; i < kUT; ++i)
 #pragma unroll
-                for (int b = 0; b < 2; ++b) {
-                    unsigned pk[4];
+                for (int b = 0; b < 2; ++b)
 #pragma unroll
                     for (int qq = 0; qq < 2; ++qq) {
                         const int q = 2 * b + qq;
@@ -505,17 +542,15 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
                         const float v1 = gelu_fast(fmaf(hacc[i][4 * q + 1], s1, bq[q].y));
                         const float v2 = gelu_fast(fmaf(hacc[i][4 * q + 2], s1, bq[q].z));
                         const float v3 = gelu_fast(fmaf(hacc[i][4 * q + 3], s1, bq[q].w));
-                        pk[2 * qq] = pack2<false>(v0, v1);
-                        pk[2 * qq + 1] = pack2<false>(v2, v3);
+                        pk[i][b][2 * qq] = pack2<false>(v0, v1);
+                        pk[i][b][2 * qq + 1] = pack2<false>(v2, v3);
                     }
-                    hv[i][b] = u32x4{pk[0], pk[1], pk[2], pk[3]};
-                }
         }
-        // every wave has finished reading the previous chunk's buffer
-        __builtin_amdgcn_s_waitcnt(0xC07F);
-        asm volatile("" ::: "memory");
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    // the chunk's hidden values into the chunk buffer, then a barrier before
+    // any wave's down phase reads them
+    auto write_h = [&]() __attribute__((always_inline)) {
         if (up_on) {
 #pragma unroll
             for (int i = 0; i < kUT; ++i)
@@ -524,17 +559,21 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
                     const int kkp = 2 * un + b;                 // down-phase k-step
                     char* dst = reinterpret_cast<char*>(sH + (kkp >> 2) * kRows * 64) +
                                 (um * 64 + i * 32 + lrow) * 128 + choff[kkp & 3];
-                    *reinterpret_cast<u32x4*>(dst) = hv[i][b];
+                    *reinterpret_cast<u32x4*>(dst) = u32x4{pk[i][b][0], pk[i][b][1], pk[i][b][2], pk[i][b][3]};
                 }
         }
         __builtin_amdgcn_s_waitcnt(0xC07F);     // lgkmcnt(0): this wave's writes are done
         asm volatile("" ::: "memory");
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        // ---- down phase: acc += h W2c^T over the chunk's 8 k-steps; the
-        // hidden fragments roll through three registers, read two row tiles
-        // ahead of their MFMAs
-        constexpr int kHQ = kDownSteps * TM;      // hidden fragments per chunk
+    };
+    // ---- down phase: acc += h W2c^T over the chunk's 8 k-steps, W2 step
+    // j at slot (base + j) % kRing; the hidden fragments roll through three
+    // registers, read two row tiles ahead of their MFMAs
+    constexpr int kHQ = kDownSteps * TM;          // hidden fragments per chunk
+    auto down_phase = [&](auto base_c, auto&& refill) __attribute__((always_inline)) {
+        constexpr int base = decltype(base_c)::value;
+        fresh_offsets();
         h8 hf[3];
         if (dn_on) {
             hf[0] = h_frag(0);
@@ -544,22 +583,44 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
         for (int q = 0; q < kHQ; ++q) {
             const int kkp = q / TM, i = q % TM;
             if (dn_on && q + 2 < kHQ) hf[(q + 2) % 3] = h_frag(q + 2);
-            const int s0 = kUpSteps + 2 * kkp;
+            const int s0 = 2 * kkp;                     // W2 step of the pair
             if (dn_on) {
                 __builtin_amdgcn_s_setprio(1);
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
-                    acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ring[(s0 + j) % kRing],
+                    acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(h8, ring[(base + s0 + j) % kRing]),
                                                                        hf[q % 3], acc[j][i], 0, 0, 0);
                 __builtin_amdgcn_s_setprio(0);
             }
             if (i == TM - 1) {
-                refill(c, s0);
-                refill(c, s0 + 1);
+                refill(s0);
+                refill(s0 + 1);
             }
             __builtin_amdgcn_sched_barrier(0);
         }
+    };
+    // every wave has finished reading the chunk buffer
+    auto sync_reads = [&]() __attribute__((always_inline)) {
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+    // block 0: chunk 0's up phase and GELU (the chunk buffer is free: the O
+    // projection's epilogue finished with it at its last barrier)
+    up_gelu(std::integral_constant<int, 0>{}, 0, refill_first);
+    write_h();
+    // block c: chunk c's up phase and GELU, then chunk c - 1's down phase.
+    // With no barrier between GELU and the down phase, a wave that finishes
+    // its GELU goes on to its MFMAs while the other wave of its SIMD may
+    // still be in GELU, so the matrix core and the vector ALUs overlap.
+    for (int c = 1; c < nch; ++c) {
+        up_gelu(std::integral_constant<int, kUpSteps>{}, c, [&](int s) { refill_mid(c, s); });
+        down_phase(std::integral_constant<int, 2 * kUpSteps>{}, [&](int s) { refill_mid(c, kUpSteps + s); });
+        sync_reads();
+        write_h();
     }
+    down_phase(std::integral_constant<int, kUpSteps>{}, refill_last);
 
     // ---- epilogue: residual update, then LayerNorm or the score head, on
     // whole rows.  Its staging regions reuse the resident rows' LDS and, for

@@ -215,3 +215,41 @@ def test_validation_errors_leave_outputs_untouched(what):
     torch.cuda.synchronize()
     assert torch.all(run.scores == 123.0)
     assert torch.equal(run.cache, cache_before)
+
+
+@pytest.mark.parametrize("d,H,F", [(128, 2, 128), (256, 4, 384), (384, 6, 256)])
+def test_fused_tail_other_widths(d, H, F):
+    """The fused layer tail at the model widths it takes besides 512 (its
+    weight ring is sized per width) and with a single hidden chunk (F = 128):
+    36,000 candidate rows make 282 tiles of 128 rows, so the batched call
+    runs the fused tail; single-user calls run the unfused pair on short
+    tiles and must agree bit for bit, and sampled candidates match the
+    oracle."""
+    rng = np.random.default_rng(d + F)
+    U = 36
+    hist = rng.integers(1, 96, size=U).tolist()
+    inp = make_inputs(hist, [1000] * U, d, H, 2, F, dtype="bf16", seed=d + F)
+    say(f"[gpu] fused tail d={d} H={H} F={F}: {int(inp.cand_offsets[-1])} candidate rows")
+    run = GpuRun(inp)
+    run.encode()
+    upr.upr_profile_enable(True)
+    run.rank()
+    batch = run.scores_np().copy()
+    prof = upr.upr_profile_read()
+    upr.upr_profile_enable(False)
+    assert "rank.oproj_ffn" in prof, f"the batched call did not run the fused tail: {sorted(prof)}"
+    assert np.all(np.isfinite(batch[: inp.cand_offsets[-1]]))
+    ho, co = inp.hist_offsets, inp.cand_offsets
+    for u in [0, U // 2, U - 1]:
+        run.scores.fill_(float("nan"))
+        run.rank(hoff=np.array([ho[u], ho[u + 1]], np.int32), coff=np.array([co[u], co[u + 1]], np.int32))
+        s = run.scores_np()
+        assert np.array_equal(s[co[u]:co[u + 1]], batch[co[u]:co[u + 1]]), f"scores of user {u}"
+    users = [0, U - 1]
+    rows = np.unique(np.concatenate([co[u] + np.sort(rng.choice(1000, size=40, replace=False))
+                                     for u in users]))
+    cache = oracle.encode(inp.weights, inp.d, inp.H, inp.L, inp.F, inp.hist_emb, ho, users=users)
+    o = oracle.rank(inp.weights, inp.d, inp.H, inp.L, inp.F, cache, ho, inp.cand_emb, co,
+                    users=users, cand_rows=rows)
+    err = assert_scores_match(batch[rows], o[rows], f"fused tail d={d} F={F}")
+    say(f"[gpu] fused tail d={d} F={F}: max |score err| {err:.3e} over {rows.size} candidates")

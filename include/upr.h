@@ -31,6 +31,12 @@
  *     offsets[0] >= 0.  User u owns packed rows offsets[u] .. offsets[u+1]-1.
  *     offsets[0] > 0 is allowed (a call on a sub-range of a shared buffer).
  *     Empty users (equal consecutive offsets) are allowed.
+ *     The device copy (offsets_dev) must hold the same values as the host
+ *     array while the call's kernels run.  The host array is what the call
+ *     validates; kernels that read the device copy check it against the
+ *     validated bounds (first and last offset, cache capacity, tile count)
+ *     and skip segments that disagree, so a stale device copy
+ *     gives meaningless outputs but no access outside the call's buffers.
  *   - A model is immutable after creation and may be used from several host
  *     threads at once; concurrent calls need distinct workspaces and must
  *     not write the same outputs.

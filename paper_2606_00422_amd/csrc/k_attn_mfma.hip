@@ -130,6 +130,7 @@ __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
     const int d = H * kD;
     const int64_t hb = hist_offsets[u];
     const int n = hist_offsets[u + 1] - hist_offsets[u];
+    if (hb < 0 || n < 0 || hb + n > cap) return;   // (only with offsets the work list rejected)
     // keys streamed: all history (ranking) or positions up to the item's
     // last query (encode); waves past the item's queries only help load
     const int ipos0 = CAUSAL ? (int)(c0 - hb) : 0;
@@ -418,12 +419,23 @@ __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
 // with H = 8 all tiles of one (user, head) share blockIdx % 8 and therefore
 // one XCD's L2.  Tiles cover the rows of `coffs` (candidates, or the history
 // itself for the causal pass).
+//
+// The offsets are read from device memory, which the caller promises holds
+// the host values the call validated.  The kernel checks that promise
+// before it writes an item: `coffs` non-decreasing from row_first to
+// row_last, `hoffs` non-decreasing within [0, cap], and the tile count equal
+// to the one sized on the host.  If any check fails, every item is written
+// empty (no queries), so the attention launches touch nothing outside the
+// call's buffers (the call's outputs are then meaningless, as the contract
+// says for inconsistent offsets).
 constexpr int kSortMax = 2048;
 
 __global__ __launch_bounds__(1024) void k_rank_worklist(const int32_t* __restrict__ coffs,
                                                         const int32_t* __restrict__ hoffs, int U,
                                                         int H, int tile, int reverse,
-                                                        int4* __restrict__ work, int64_t items) {
+                                                        int4* __restrict__ work, int64_t items,
+                                                        int64_t row_first, int64_t row_last,
+                                                        int64_t cap) {
     __shared__ int s_len[kSortMax];
     __shared__ int s_tiles[kSortMax];     // tiles of the user at each rank
     __shared__ int s_user[kSortMax];      // user at each rank
@@ -431,6 +443,28 @@ __global__ __launch_bounds__(1024) void k_rank_worklist(const int32_t* __restric
     __shared__ int s_cu[1024];            // user of each rank of the chunk
     __shared__ long long s_carry;
     const int tid = threadIdx.x;
+    {
+        bool bad = false;
+        long long tiles = 0;
+        for (int u = tid; u < U; u += 1024) {
+            const int64_t c0 = coffs[u], c1 = coffs[u + 1], h0 = hoffs[u], h1 = hoffs[u + 1];
+            bad |= c1 < c0 || h0 < 0 || h1 < h0 || h1 > cap;
+            if (c1 >= c0) tiles += (c1 - c0 + tile - 1) / tile;
+        }
+        if (tid == 0) bad |= coffs[0] != row_first || coffs[U] != row_last;
+        // the tile total, reduced over the workgroup through LDS
+        s_scan[tid] = (int)min(tiles, (long long)(1 << 30));
+        __syncthreads();
+        for (int off = 512; off > 0; off >>= 1) {
+            if (tid < off) s_scan[tid] = (int)min((long long)s_scan[tid] + s_scan[tid + off], (long long)(1 << 30));
+            __syncthreads();
+        }
+        if (tid == 0) bad |= (long long)s_scan[0] * H != items;
+        if (__syncthreads_or(bad)) {
+            for (int64_t i = tid; i < items; i += 1024) work[i] = make_int4(0, 0, 0, 0);
+            return;
+        }
+    }
     const bool sorted = U <= kSortMax;
     if (sorted) {
         for (int u = tid; u < U; u += 1024) s_len[u] = hoffs[u + 1] - hoffs[u];
@@ -498,10 +532,10 @@ __global__ __launch_bounds__(1024) void k_rank_worklist(const int32_t* __restric
 
 hipError_t launch_attn_worklist(const int32_t* row_offsets, const int32_t* hist_offsets, int U,
                                 int H, int tile, bool reverse, int32_t* work, int64_t items,
-                                hipStream_t s) {
+                                int64_t row_first, int64_t row_last, int64_t cap, hipStream_t s) {
     if (items == 0) return hipSuccess;
     k_rank_worklist<<<1, 1024, 0, s>>>(row_offsets, hist_offsets, U, H, tile, reverse ? 1 : 0,
-                                       reinterpret_cast<int4*>(work), items);
+                                       reinterpret_cast<int4*>(work), items, row_first, row_last, cap);
     return hipGetLastError();
 }
 

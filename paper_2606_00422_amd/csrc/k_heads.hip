@@ -99,11 +99,15 @@ __device__ __forceinline__ uint64_t topk_key(float f, uint32_t local_row) {
 __global__ __launch_bounds__(kTopkThreads) void k_topk(const float* __restrict__ util,
                                                        const int32_t* __restrict__ coffs, int K,
                                                        int32_t* __restrict__ out_rows,
-                                                       float* __restrict__ out_util) {
+                                                       float* __restrict__ out_util, int64_t row_first,
+                                                       int64_t row_last) {
     __shared__ uint64_t keys[kTopkMaxCandidates];
     const int u = blockIdx.x, tid = threadIdx.x;
     const int32_t r0 = coffs[u];
-    const int k = coffs[u + 1] - r0;
+    int k = coffs[u + 1] - r0;
+    // device offsets that disagree with the validated host ones (a caller
+    // error): no entries rather than reads outside the utility rows
+    if (r0 < row_first || k < 0 || r0 + (int64_t)k > row_last || k > kTopkMaxCandidates) k = 0;
     int N = 1;
     while (N < k) N <<= 1;
     for (int i = tid; i < N; i += kTopkThreads)
@@ -150,10 +154,12 @@ hipError_t launch_heads_out(const TA* hid, int64_t ldh, int64_t rows, int C, int
 }
 
 hipError_t launch_topk(const float* util, const int32_t* coffs_dev, int U, int K,
-                       int32_t* out_rows, float* out_util, hipStream_t s) {
+                       int32_t* out_rows, float* out_util, int64_t row_first, int64_t row_last,
+                       hipStream_t s) {
     if (U == 0) return hipSuccess;
     if (K < 1) return hipErrorInvalidValue;
-    k_topk<<<(unsigned)U, kTopkThreads, 0, s>>>(util, coffs_dev, K, out_rows, out_util);
+    k_topk<<<(unsigned)U, kTopkThreads, 0, s>>>(util, coffs_dev, K, out_rows, out_util, row_first,
+                                                row_last);
     return hipGetLastError();
 }
 

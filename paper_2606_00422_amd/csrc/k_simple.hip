@@ -101,7 +101,10 @@ __global__ __launch_bounds__(256) void k_attn_rank_simple(
     if (r >= rows) return;
     const int u = find_segment(cand_offsets, U, r + row0);
     const int64_t hb = hist_offsets[u];
-    const int n = hist_offsets[u + 1] - hist_offsets[u];
+    int n = hist_offsets[u + 1] - hist_offsets[u];
+    // device offsets that disagree with the validated host ones (a caller
+    // error) must not move the key range outside the cache
+    if (hb < 0 || n < 0 || hb + n > cap) n = 0;
     const int d = H * D;
     const T* qrow = qkv + r * 3 * d + h * D;
     float q[D];
@@ -165,7 +168,8 @@ __global__ __launch_bounds__(256) void k_attn_encode_simple(
     const int64_t arow = r + row0;
     const int u = find_segment(hist_offsets, U, arow);
     const int64_t hb = hist_offsets[u];
-    const int i = (int)(arow - hb);
+    // (-1, no keys, for device offsets that disagree with the host ones)
+    const int i = hb < 0 || arow < hb || arow >= cap ? -1 : (int)(arow - hb);
     const int d = H * D;
     const T* qrow = qbuf + r * d + h * D;
     float q[D];

@@ -350,7 +350,8 @@ static upr_status rank_layers_mx(const upr_model* m, const upr_kv_cache* cache,
         UPR_LAUNCH("rank.worklist",
                    launch_attn_worklist(cand->offsets_dev, hist->offsets_dev, cand->num_users, H,
                                         p.attn_tile, false, reinterpret_cast<int32_t*>(ws + p.off_work),
-                                        p.work_items, s));
+                                        p.work_items, cand->offsets_host[0],
+                                        cand->offsets_host[cand->num_users], cache->capacity_rows, s));
     // LN2 is folded into the O projection (EPI_RESID_LN_MX) when a row fits
     // its tile; it then writes LN2 over its own operand (the attention
     // output): each tile owns whole rows and overwrites them after its last
@@ -563,7 +564,8 @@ static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_
         UPR_LAUNCH("encode.worklist",
                    launch_attn_worklist(hist->offsets_dev, hist->offsets_dev, hist->num_users, H,
                                         p.attn_tile, true, reinterpret_cast<int32_t*>(ws + p.off_work),
-                                        p.work_items, s));
+                                        p.work_items, hist->offsets_host[0],
+                                        hist->offsets_host[hist->num_users], cache->capacity_rows, s));
     for (int l = 0; l < c.n_layers; ++l) {
         const LayerWeights& w = m->layers[l];
         if (l > 0 && !fused_layernorm<Types>(c))
@@ -657,7 +659,8 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
     if (p.use_mfma_attn)
         UPR_LAUNCH("rank.worklist", launch_attn_worklist(cand->offsets_dev, hist->offsets_dev, cand->num_users, H,
                                      p.attn_tile, false, reinterpret_cast<int32_t*>(ws + p.off_work),
-                                     p.work_items, s));
+                                     p.work_items, cand->offsets_host[0],
+                                     cand->offsets_host[cand->num_users], cache->capacity_rows, s));
     for (int l = 0; l < c.n_layers; ++l) {
         const LayerWeights& w = m->layers[l];
         if (l > 0 && !fused_layernorm<Types>(c))
@@ -1155,7 +1158,7 @@ upr_status upr_topk_by_utility(const float* utility, const upr_segments* cand, i
     {
         upr::ProfScope ps("topk", s);
         const hipError_t e = upr::launch_topk(utility, cand->offsets_dev, cand->num_users, K,
-                                              topk_rows, topk_utility, s);
+                                              topk_rows, topk_utility, cf, cl, s);
         if (e != hipSuccess) return fail(UPR_ERR_HIP, "top-K launch failed: %s", hipGetErrorString(e));
     }
     return ok();

@@ -145,9 +145,11 @@ hipError_t launch_ffn_fused(const f16* O, const f16* WoP, const Epilogue& epa, c
 // query count) over the rows of `row_offsets` (candidates, or the history
 // itself for encode), users with the longest history first; `reverse` lists
 // each user's tiles last-first (encode: the costliest causal tiles first).
+// row_first / row_last: the host values of row_offsets[0] and [U]; cap: the
+// cache rows.  Device offsets that disagree with them yield empty items.
 hipError_t launch_attn_worklist(const int32_t* row_offsets, const int32_t* hist_offsets, int U,
                                 int H, int tile, bool reverse, int32_t* work, int64_t items,
-                                hipStream_t s);
+                                int64_t row_first, int64_t row_last, int64_t cap, hipStream_t s);
 
 // MFMA ranking attention (bf16 q|k|v rows and cache, head_dim 64), fp16 output.
 hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
@@ -189,9 +191,11 @@ hipError_t launch_heads_out(const TA* hid, int64_t ldh, int64_t rows, int C, int
                             float* util, hipStream_t s);
 
 // Per-user top K by utility (one workgroup per user, at most
-// kTopkMaxCandidates candidates per user: the caller checks).
+// kTopkMaxCandidates candidates per user: the caller checks).  A user whose
+// device offsets leave [row_first, row_last] or that limit gets no entries.
 constexpr int kTopkMaxCandidates = 16384;
 hipError_t launch_topk(const float* util, const int32_t* coffs_dev, int U, int K,
-                       int32_t* out_rows, float* out_util, hipStream_t s);
+                       int32_t* out_rows, float* out_util, int64_t row_first, int64_t row_last,
+                       hipStream_t s);
 
 }  // namespace upr

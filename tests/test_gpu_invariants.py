@@ -253,3 +253,34 @@ def test_fused_tail_other_widths(d, H, F):
                     users=users, cand_rows=rows)
     err = assert_scores_match(batch[rows], o[rows], f"fused tail d={d} F={F}")
     say(f"[gpu] fused tail d={d} F={F}: max |score err| {err:.3e} over {rows.size} candidates")
+
+
+def test_device_offsets_that_disagree_are_skipped():
+    """The device copy of the candidate offsets disagrees with the host array
+    (a caller error the contract rules out).  The values are chosen so that
+    every access would stay inside the buffers even if they were used as
+    given (the device split has more tiles than the host one, and the work
+    list holds at most the host count), so the case is safe either way; the
+    work list's check must reject them and leave every item empty.  The
+    attention then writes nothing, so the scores follow whatever the
+    workspace held, while with a consistent device copy they do not depend
+    on it."""
+    import torch
+    inp = make_inputs([50, 30], [300, 0], 256, 4, 1, 512, dtype="bf16", seed=5)
+    say("[gpu] device offsets that disagree with the host ones")
+    run = GpuRun(inp)
+    run.encode()
+    stale = torch.from_numpy(np.array([0, 1, 300], np.int32)).to("cuda")
+    ws = run.model.rank(run.cache, run.hoff, run.hoff_d, run.C, run.coff, run.coff_d, run.scores)
+
+    def scores_with(fill, cand_dev):
+        ws.fill_(fill)
+        run.scores.fill_(float("nan"))
+        run.model.rank(run.cache, run.hoff, run.hoff_d, run.C, run.coff, cand_dev, run.scores, ws=ws)
+        return run.scores_np()[:300].copy()
+
+    good0, good1 = scores_with(0, run.coff_d), scores_with(0x3C, run.coff_d)
+    assert np.array_equal(good0, good1), "a consistent call read workspace bytes it did not write"
+    bad0, bad1 = scores_with(0, stale), scores_with(0x3C, stale)
+    assert np.all(np.isfinite(bad0)) and np.all(np.isfinite(bad1))
+    assert not np.array_equal(bad0, bad1), "the attention ran on offsets the check should reject"

@@ -69,8 +69,8 @@ constexpr int kFC = 128;              // hidden columns per chunk
 constexpr int kMaxD = 512;            // widest row (the tile spans whole rows)
 // Weight fragments in flight per wave, by K-blocks of the up phase: as deep
 // as the 256 registers of two waves per SIMD allow, and a divisor of the
-// fragments per chunk (4 KB + 16), so a slot refilled with the next chunk's
-// fragment is the slot that fragment is read from.
+// fragments per block of the stream (4 KB + 16), so a step's slot depends
+// only on its place in its block.
 template <int KB>
 constexpr int ring_depth() { return KB == 8 ? 6 : KB == 6 ? 5 : 8; }
 constexpr int kDownSteps = kFC / 16;  // k-steps of the down phase per chunk (8)
@@ -267,10 +267,10 @@ __global__ __launch_bounds__(512, 1) void k_ffn_fused(const f16* __restrict__ O,
     constexpr int kRows = 32 * TM;
     constexpr int kD = 64 * KB;
     constexpr int kUpSteps = 4 * KB;                   // 16-deep k-steps of the up phase
-    constexpr int kSteps = kUpSteps + 2 * kDownSteps;  // weight fragments per chunk
+    constexpr int kSteps = kUpSteps + 2 * kDownSteps;  // weight fragments per chunk (and per block)
     constexpr int kUT = TM >= 2 ? TM / 2 : 1;          // up-phase row tiles per wave
     constexpr int kRing = ring_depth<KB>();
-    static_assert(kSteps % kRing == 0 && kRing <= kUpSteps, "ring slots repeat every chunk");
+    static_assert(kSteps % kRing == 0 && kRing <= kUpSteps, "ring slots repeat every block");
     __shared__ __attribute__((aligned(16))) char smem[smem_bytes<TM>()];
     f16* const sA = reinterpret_cast<f16*>(smem);                          // [KB][kRows x 64]
     f16* const sH = reinterpret_cast<f16*>(smem + kRows * kMaxD * 2);      // [2][kRows x 64]

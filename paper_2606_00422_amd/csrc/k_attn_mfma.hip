@@ -135,8 +135,10 @@ __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
     // last query (encode); waves past the item's queries only help load
     const int ipos0 = CAUSAL ? (int)(c0 - hb) : 0;
     const int nkeys = CAUSAL ? ipos0 + kc : n;
-    const bool wave_active = wave * kQW < kc;
-    const int wave_last = ipos0 + min(wave * kQW + kQW, kc) - 1;   // encode: last query position
+    // (wave-uniform values made scalar, so the per-wave skips are scalar
+    // branches rather than exec-mask updates)
+    const bool wave_active = __builtin_amdgcn_readfirstlane((int)(wave * kQW < kc)) != 0;
+    const int wave_last = __builtin_amdgcn_readfirstlane(ipos0 + min(wave * kQW + kQW, kc) - 1);
 
     // ---- queries of this wave (B operand of S^T), own key/value, initial state
     b8 qf[kQG][2];

@@ -139,6 +139,7 @@ __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
     // branches rather than exec-mask updates)
     const bool wave_active = __builtin_amdgcn_readfirstlane((int)(wave * kQW < kc)) != 0;
     const int wave_last = __builtin_amdgcn_readfirstlane(ipos0 + min(wave * kQW + kQW, kc) - 1);
+    const int wave_first = __builtin_amdgcn_readfirstlane(ipos0 + wave * kQW);   // encode: first query position
 
     // ---- queries of this wave (B operand of S^T), own key/value, initial state
     b8 qf[kQG][2];
@@ -246,7 +247,7 @@ __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
         __builtin_amdgcn_s_setprio(0);
         // ranking: mask keys past the history end (last sub-block only);
         // encode: mask keys after the query (diagonal sub-blocks only)
-        if (__builtin_expect(CAUSAL ? kabs + 31 > ipos0 + wave * kQW : kabs + 32 > n, 0)) {
+        if (__builtin_expect(CAUSAL ? kabs + 31 > wave_first : kabs + 32 > n, 0)) {
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll

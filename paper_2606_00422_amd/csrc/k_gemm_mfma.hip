@@ -488,4 +488,11 @@ hipError_t launch_gemm_mx(const uint8_t* A, const uint8_t* A_scales, const uint8
     }
 }
 
+// bf16 models: fp16 projection operands on the matrix cores
+template <>
+hipError_t launch_gemm<f16, bf16>(const f16* A, int64_t lda, const f16* W, int64_t M, int N,
+                                  int K, const Epilogue& epi, hipStream_t s) {
+    return launch_gemm_mfma(A, lda, W, M, N, K, epi, s);
+}
+
 }  // namespace upr

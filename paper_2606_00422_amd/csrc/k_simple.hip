@@ -7,6 +7,7 @@
 
 #include "epilogue.h"
 #include "upr_internal.h"
+#include "upr_plan.h"
 
 namespace upr {
 
@@ -264,6 +265,14 @@ hipError_t launch_attn_encode_simple(const TKV* q, TA* o, int64_t rows, int64_t 
 UPR_INST(float, float)
 UPR_INST(bf16, f16)
 #undef UPR_INST
+// fp32 models: every projection runs on the FMA GEMM (fp32 residual rows only)
+template <>
+hipError_t launch_gemm<float, float>(const float* A, int64_t lda, const float* W, int64_t M,
+                                     int N, int K, const Epilogue& epi, hipStream_t s) {
+    if (epi.resid_src != nullptr) return hipErrorInvalidValue;
+    return launch_gemm_simple<float, float>(A, lda, W, M, N, K, epi, s);
+}
+
 // the fp8 projection variant's fallback attention: bf16 queries/keys/values
 // and cache, fp32 output for the MXFP8 encoder
 template hipError_t launch_attn_rank_simple<bf16, float>(const bf16*, float*, int64_t, int64_t,

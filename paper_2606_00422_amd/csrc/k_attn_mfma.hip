@@ -110,8 +110,7 @@ __device__ __forceinline__ float quad_sum(float v) {
 template <bool CAUSAL, int kQG, bool MXO = false>
 __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
     const bf16* __restrict__ qsrc, int64_t qstride, void* __restrict__ out,
-    uint8_t* __restrict__ out_scales, int64_t row0, int H,
-    const int32_t* __restrict__ hist_offsets, const int4* __restrict__ work,
+    uint8_t* __restrict__ out_scales, int64_t row0, int H, const int4* __restrict__ work,
     const bf16* __restrict__ cache_k, const bf16* __restrict__ cache_v, int64_t cap, int force_exact) {
     // Stages as separate arrays: the compiler can then tell that reads of one
     // stage do not alias the loads filling the other.
@@ -121,16 +120,18 @@ __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
     __shared__ __attribute__((aligned(16))) bf16 sV1[kKS * kD];
 
     constexpr int kQW = 16 * kQG;       // queries per wave
+    // the item carries its user's history segment, so nothing here waits on
+    // a second dependent load before the first K/V stage can be requested
     const int4 item = work[blockIdx.x];
-    const int u = item.x, h = item.y, kc = item.w;
+    const int h = item.w & 0xffff, kc = item.w >> 16;
     if (kc <= 0) return;
     const int64_t c0 = item.z;          // absolute row of the first query
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, l16 = lane & 15;
     const int d = H * kD;
-    const int64_t hb = hist_offsets[u];
-    const int n = hist_offsets[u + 1] - hist_offsets[u];
-    if (hb < 0 || n < 0 || hb + n > cap) return;   // (only with offsets the work list rejected)
+    const int64_t hb = item.x;
+    const int n = item.y;
+    if (hb < 0 || n < 0 || hb + n > cap) return;   // (never, for an item of the work list)
     // keys streamed: all history (ranking) or positions up to the item's
     // last query (encode); waves past the item's queries only help load
     const int ipos0 = CAUSAL ? (int)(c0 - hb) : 0;
@@ -140,6 +141,40 @@ __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
     const bool wave_active = __builtin_amdgcn_readfirstlane((int)(wave * kQW < kc)) != 0;
     const int wave_last = __builtin_amdgcn_readfirstlane(ipos0 + min(wave * kQW + kQW, kc) - 1);
     const int wave_first = __builtin_amdgcn_readfirstlane(ipos0 + wave * kQW);   // encode: first query position
+
+    // ---- history K/V stages, loaded straight into LDS.  Buffer descriptors
+    // span the user's n rows, so rows past the history end read as zeros.
+    const int nst = (nkeys + kKS - 1) / kKS;
+    const __amdgpu_buffer_rsrc_t rsK = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(cache_k + ((int64_t)h * cap + hb) * kD), (short)0, n * kD * 2, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rsV = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(cache_v + ((int64_t)h * cap + hb) * kD), (short)0, n * kD * 2, 0x00020000);
+    // Wave w fills rows 16w .. 16w+15 of a stage with two 8-row loads per
+    // matrix; slot s of row r holds logical chunk s ^ key(r).
+    int offK[2], offV[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int row = 16 * wave + 8 * i + (lane >> 3), slot = lane & 7;
+        offK[i] = row * kD * 2 + ((slot ^ key_k(row)) << 4);
+        offV[i] = row * kD * 2 + ((slot ^ key_v(row)) << 4);
+    }
+    auto issue_loads = [&](bf16* dK, bf16* dV, int st) __attribute__((always_inline)) {
+        const int base = st * kKS * kD * 2;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rsK, (__attribute__((address_space(3))) void*)(dK + (16 * wave + 8 * i) * kD),
+                16, offK[i] + base, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rsV, (__attribute__((address_space(3))) void*)(dV + (16 * wave + 8 * i) * kD),
+                16, offV[i] + base, 0, 0, 0);
+        }
+    };
+
+    // The first stage is requested before the queries are loaded, so the two
+    // latencies overlap.
+    bool first_issued = nst > 0;
+    if (first_issued) issue_loads(sK0, sV0, 0);
 
     // ---- queries of this wave (B operand of S^T), own key/value, initial state
     b8 qf[kQG][2];
@@ -193,35 +228,6 @@ __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
         for (int qg = 0; qg < kQG; ++qg) none[qg] = -INFINITY;
         init_state(none);
     }
-
-    // ---- history K/V stages, loaded straight into LDS.  Buffer descriptors
-    // span the user's n rows, so rows past the history end read as zeros.
-    const int nst = (nkeys + kKS - 1) / kKS;
-    const __amdgpu_buffer_rsrc_t rsK = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(cache_k + ((int64_t)h * cap + hb) * kD), (short)0, n * kD * 2, 0x00020000);
-    const __amdgpu_buffer_rsrc_t rsV = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(cache_v + ((int64_t)h * cap + hb) * kD), (short)0, n * kD * 2, 0x00020000);
-    // Wave w fills rows 16w .. 16w+15 of a stage with two 8-row loads per
-    // matrix; slot s of row r holds logical chunk s ^ key(r).
-    int offK[2], offV[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int row = 16 * wave + 8 * i + (lane >> 3), slot = lane & 7;
-        offK[i] = row * kD * 2 + ((slot ^ key_k(row)) << 4);
-        offV[i] = row * kD * 2 + ((slot ^ key_v(row)) << 4);
-    }
-    auto issue_loads = [&](bf16* dK, bf16* dV, int st) __attribute__((always_inline)) {
-        const int base = st * kKS * kD * 2;
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rsK, (__attribute__((address_space(3))) void*)(dK + (16 * wave + 8 * i) * kD),
-                16, offK[i] + base, 0, 0, 0);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rsV, (__attribute__((address_space(3))) void*)(dV + (16 * wave + 8 * i) * kD),
-                16, offV[i] + base, 0, 0, 0);
-        }
-    };
 
     // One 32-key sub-block (keys kb .. kb+31 of the stage in cK / cV).
     auto sub_block = [&](const bf16* cK, const bf16* cV, int kb, int kabs) __attribute__((always_inline)) {
@@ -307,7 +313,8 @@ __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
 
     auto run = [&]() __attribute__((always_inline)) {
         if (nst > 0) {
-            issue_loads(sK0, sV0, 0);
+            if (!first_issued) issue_loads(sK0, sV0, 0);    // (the exact redo's second pass)
+            first_issued = false;
             __builtin_amdgcn_s_waitcnt(0x0F70);
         }
         __syncthreads();
@@ -421,7 +428,8 @@ __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
 // `reverse`: the causal pass puts a user's costliest, last tiles first), so
 // with H = 8 all tiles of one (user, head) share blockIdx % 8 and therefore
 // one XCD's L2.  Tiles cover the rows of `coffs` (candidates, or the history
-// itself for the causal pass).
+// itself for the causal pass).  An item is (first history row of its user,
+// history length, first query row, head | query count << 16).
 //
 // The offsets are read from device memory, which the caller promises holds
 // the host values the call validated.  The kernel checks that promise
@@ -522,7 +530,8 @@ __global__ __launch_bounds__(1024) void k_rank_worklist(const int32_t* __restric
                 const int k = coffs[ur + 1] - coffs[ur];
                 const int tt = reverse ? tr - 1 - j : j;
                 const int cnt = min(tile, k - tt * tile);
-                work[idx] = make_int4(ur, hh, coffs[ur] + tt * tile, cnt);
+                work[idx] = make_int4(hoffs[ur], hoffs[ur + 1] - hoffs[ur], coffs[ur] + tt * tile,
+                                      hh | (cnt << 16));
             }
         }
         __syncthreads();
@@ -550,24 +559,24 @@ static int force_exact_flag() {
 }
 
 hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
-                            const int32_t* hist_offsets, const int32_t* work, int64_t items,
+                            const int32_t* work, int64_t items,
                             int tile, const bf16* cache_k, const bf16* cache_v, int64_t cache_cap,
                             hipStream_t s) {
     if (items == 0) return hipSuccess;
     if (D != kD || (tile != kRankAttnTile && tile != kSmallRankAttnTile)) return hipErrorInvalidValue;
     if (tile == kRankAttnTile)
         k_attn_mfma<false, kRankQG><<<(unsigned)items, 256, 0, s>>>(
-            qkv, (int64_t)3 * H * kD, o, nullptr, row0, H, hist_offsets,
+            qkv, (int64_t)3 * H * kD, o, nullptr, row0, H,
             reinterpret_cast<const int4*>(work), cache_k, cache_v, cache_cap, force_exact_flag());
     else
         k_attn_mfma<false, kSmallRankQG><<<(unsigned)items, 256, 0, s>>>(
-            qkv, (int64_t)3 * H * kD, o, nullptr, row0, H, hist_offsets,
+            qkv, (int64_t)3 * H * kD, o, nullptr, row0, H,
             reinterpret_cast<const int4*>(work), cache_k, cache_v, cache_cap, force_exact_flag());
     return hipGetLastError();
 }
 
 hipError_t launch_attn_rank_mx(const bf16* qkv, uint8_t* codes, uint8_t* scales, int64_t row0,
-                               int H, int D, const int32_t* hist_offsets, const int32_t* work,
+                               int H, int D, const int32_t* work,
                                int64_t items, int tile, const bf16* cache_k, const bf16* cache_v,
                                int64_t cache_cap, hipStream_t s) {
     if (items == 0) return hipSuccess;
@@ -575,23 +584,23 @@ hipError_t launch_attn_rank_mx(const bf16* qkv, uint8_t* codes, uint8_t* scales,
         return hipErrorInvalidValue;
     if (tile == kRankAttnTile)
         k_attn_mfma<false, kRankQG, true><<<(unsigned)items, 256, 0, s>>>(
-            qkv, (int64_t)3 * H * kD, codes, scales, row0, H, hist_offsets,
+            qkv, (int64_t)3 * H * kD, codes, scales, row0, H,
             reinterpret_cast<const int4*>(work), cache_k, cache_v, cache_cap, force_exact_flag());
     else
         k_attn_mfma<false, kSmallRankQG, true><<<(unsigned)items, 256, 0, s>>>(
-            qkv, (int64_t)3 * H * kD, codes, scales, row0, H, hist_offsets,
+            qkv, (int64_t)3 * H * kD, codes, scales, row0, H,
             reinterpret_cast<const int4*>(work), cache_k, cache_v, cache_cap, force_exact_flag());
     return hipGetLastError();
 }
 
 hipError_t launch_attn_encode(const bf16* q, f16* o, int64_t row0, int H, int D,
-                              const int32_t* hist_offsets, const int32_t* work, int64_t items,
+                              const int32_t* work, int64_t items,
                               int tile, const bf16* cache_k, const bf16* cache_v,
                               int64_t cache_cap, hipStream_t s) {
     if (items == 0) return hipSuccess;
     if (D != kD || tile != kAttnTile) return hipErrorInvalidValue;
     k_attn_mfma<true, kEncodeQG><<<(unsigned)items, 256, 0, s>>>(
-        q, (int64_t)H * kD, o, nullptr, row0, H, hist_offsets, reinterpret_cast<const int4*>(work), cache_k,
+        q, (int64_t)H * kD, o, nullptr, row0, H, reinterpret_cast<const int4*>(work), cache_k,
         cache_v, cache_cap, force_exact_flag());
     return hipGetLastError();
 }

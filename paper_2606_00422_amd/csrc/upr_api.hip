@@ -392,7 +392,7 @@ static upr_status rank_layers_mx(const upr_model* m, const upr_kv_cache* cache,
         const bf16* cv = static_cast<const bf16*>(plane_ptr(c, cache, l, 1));
         if (p.use_mfma_attn) {
             // attention writes the O projection's MXFP8 operand directly
-            UPR_LAUNCH("rank.attn", launch_attn_rank_mx(qkv, ac, asc, p.row0, H, D, hist->offsets_dev,
+            UPR_LAUNCH("rank.attn", launch_attn_rank_mx(qkv, ac, asc, p.row0, H, D,
                                                         reinterpret_cast<const int32_t*>(ws + p.off_work),
                                                         p.work_items, p.attn_tile, ck, cv,
                                                         cache->capacity_rows, s));
@@ -592,7 +592,7 @@ static upr_status run_encode(const upr_model* m, const typename Types::kv* hist_
         if constexpr (std::is_same_v<Types, Bf16Types>) {
             if (p.use_mfma_attn) {
                 UPR_LAUNCH("encode.attn",
-                           launch_attn_encode(q, o, p.row0, H, D, hist->offsets_dev,
+                           launch_attn_encode(q, o, p.row0, H, D,
                                               reinterpret_cast<const int32_t*>(ws + p.off_work),
                                               p.work_items, p.attn_tile,
                                               static_cast<const T*>(e.cache_k),
@@ -680,7 +680,7 @@ static upr_status run_rank(const upr_model* m, const upr_kv_cache* cache,
         bool done = false;
         if constexpr (std::is_same_v<Types, Bf16Types>) {
             if (p.use_mfma_attn) {
-                UPR_LAUNCH("rank.attn", launch_attn_rank(qkv, o, p.row0, H, D, hist->offsets_dev,
+                UPR_LAUNCH("rank.attn", launch_attn_rank(qkv, o, p.row0, H, D,
                                          reinterpret_cast<const int32_t*>(ws + p.off_work),
                                          p.work_items, p.attn_tile, ck, cv, cache->capacity_rows,
                                          s));

@@ -141,9 +141,10 @@ hipError_t launch_ffn_fused(const f16* O, const f16* WoP, const Epilogue& epa, c
                             const f16* W2p, const float* b1, float s1, int64_t M, int d, int F,
                             const Epilogue& epi, hipStream_t s);
 
-// Work list of the MFMA attention: entries (user, head, first query row,
-// query count) over the rows of `row_offsets` (candidates, or the history
-// itself for encode), users with the longest history first; `reverse` lists
+// Work list of the MFMA attention: entries (first history row of the user,
+// history length, first query row, head | query count << 16) over the rows
+// of `row_offsets` (candidates, or the history itself for encode), users
+// with the longest history first; `reverse` lists
 // each user's tiles last-first (encode: the costliest causal tiles first).
 // row_first / row_last: the host values of row_offsets[0] and [U]; cap: the
 // cache rows.  Device offsets that disagree with them yield empty items.
@@ -153,7 +154,7 @@ hipError_t launch_attn_worklist(const int32_t* row_offsets, const int32_t* hist_
 
 // MFMA ranking attention (bf16 q|k|v rows and cache, head_dim 64), fp16 output.
 hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
-                            const int32_t* hist_offsets, const int32_t* work, int64_t items,
+                            const int32_t* work, int64_t items,
                             int tile, const bf16* cache_k, const bf16* cache_v, int64_t cache_cap,
                             hipStream_t s);
 
@@ -161,14 +162,14 @@ hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
 // per 32-value block [rows, H*2]), encoded from the normalised fp32 values:
 // the fp8 projection variant's input of the O projection.
 hipError_t launch_attn_rank_mx(const bf16* qkv, uint8_t* codes, uint8_t* scales, int64_t row0,
-                               int H, int D, const int32_t* hist_offsets, const int32_t* work,
+                               int H, int D, const int32_t* work,
                                int64_t items, int tile, const bf16* cache_k, const bf16* cache_v,
                                int64_t cache_cap, hipStream_t s);
 
 // MFMA causal encode attention (bf16 query rows and cache, head_dim 64),
 // fp16 output.
 hipError_t launch_attn_encode(const bf16* q, f16* o, int64_t row0, int H, int D,
-                              const int32_t* hist_offsets, const int32_t* work, int64_t items,
+                              const int32_t* work, int64_t items,
                               int tile, const bf16* cache_k, const bf16* cache_v,
                               int64_t cache_cap, hipStream_t s);
 

@@ -10,7 +10,9 @@
 // Queries are pre-scaled by log2(e)/sqrt(D), so the softmax uses exp2.
 //
 // One workgroup = one work item (user, head, up to 128 candidates or 128
-// history rows); four waves of 32 queries.  The
+// history rows); four waves of 32 queries (ranking calls over long
+// histories: 256 candidates, eight waves, so each K/V stage serves twice the
+// queries; calls too small to fill the device: 64 candidates).  The
 // user's cached K/V for this layer and head are
 // streamed through LDS in 64-key stages (double-buffered, loaded straight
 // from global memory into LDS) and shared by all queries of the item.  Per
@@ -61,6 +63,7 @@ constexpr int kKS = 64;           // keys per LDS stage
 // SIMD, read half the K/V per query but measured 26% slower)
 constexpr int kRankQG = 2, kSmallRankQG = 1, kEncodeQG = 2;
 static_assert(4 * 16 * kRankQG == kRankAttnTile, "ranking work-list tile must match the kernel");
+static_assert(8 * 16 * kRankQG == kLongRankAttnTile, "long-history tile: eight waves of 32 queries");
 static_assert(4 * 16 * kSmallRankQG == kSmallRankAttnTile, "small-call tile must match the kernel");
 static_assert(4 * 16 * kEncodeQG == kAttnTile, "encode work-list tile must match the kernel");
 
@@ -107,8 +110,8 @@ __device__ __forceinline__ float quad_sum(float v) {
 // MXO: the output goes out as MXFP8 (codes in `out`, one E8M0 byte per
 // 32-value block in `out_scales`), encoded from the fp32 values, for the fp8
 // projection variant; else fp16.
-template <bool CAUSAL, int kQG, bool MXO = false>
-__global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
+template <bool CAUSAL, int kQG, bool MXO = false, int kW = 4>
+__global__ __launch_bounds__(64 * kW, kW == 8 ? 2 : (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
     const bf16* __restrict__ qsrc, int64_t qstride, void* __restrict__ out,
     uint8_t* __restrict__ out_scales, int64_t row0, int H, const int4* __restrict__ work,
     const bf16* __restrict__ cache_k, const bf16* __restrict__ cache_v, int64_t cap, int force_exact) {
@@ -149,24 +152,29 @@ __global__ __launch_bounds__(256, (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
         (void*)(cache_k + ((int64_t)h * cap + hb) * kD), (short)0, n * kD * 2, 0x00020000);
     const __amdgpu_buffer_rsrc_t rsV = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(cache_v + ((int64_t)h * cap + hb) * kD), (short)0, n * kD * 2, 0x00020000);
-    // Wave w fills rows 16w .. 16w+15 of a stage with two 8-row loads per
-    // matrix; slot s of row r holds logical chunk s ^ key(r).
+    // Each of the kW waves fills kRPW rows of a stage (wave w: rows kRPW w ..)
+    // with 8-row loads, two per matrix (four waves) or one (eight); slot s of
+    // row r holds logical chunk s ^ key(r).  (Fixed-size arrays: with a
+    // template-dependent size the host pass of this compiler drops the
+    // kernel's launch stub.)
+    constexpr int kRPW = kKS / kW, kLPM = kRPW / 8;
+    static_assert(kLPM == 1 || kLPM == 2, "four or eight waves");
     int offK[2], offV[2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int row = 16 * wave + 8 * i + (lane >> 3), slot = lane & 7;
+    for (int i = 0; i < kLPM; ++i) {
+        const int row = kRPW * wave + 8 * i + (lane >> 3), slot = lane & 7;
         offK[i] = row * kD * 2 + ((slot ^ key_k(row)) << 4);
         offV[i] = row * kD * 2 + ((slot ^ key_v(row)) << 4);
     }
     auto issue_loads = [&](bf16* dK, bf16* dV, int st) __attribute__((always_inline)) {
         const int base = st * kKS * kD * 2;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+        for (int i = 0; i < kLPM; ++i) {
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rsK, (__attribute__((address_space(3))) void*)(dK + (16 * wave + 8 * i) * kD),
+                rsK, (__attribute__((address_space(3))) void*)(dK + (kRPW * wave + 8 * i) * kD),
                 16, offK[i] + base, 0, 0, 0);
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rsV, (__attribute__((address_space(3))) void*)(dV + (16 * wave + 8 * i) * kD),
+                rsV, (__attribute__((address_space(3))) void*)(dV + (kRPW * wave + 8 * i) * kD),
                 16, offV[i] + base, 0, 0, 0);
         }
     };
@@ -563,15 +571,19 @@ hipError_t launch_attn_rank(const bf16* qkv, f16* o, int64_t row0, int H, int D,
                             int tile, const bf16* cache_k, const bf16* cache_v, int64_t cache_cap,
                             hipStream_t s) {
     if (items == 0) return hipSuccess;
-    if (D != kD || (tile != kRankAttnTile && tile != kSmallRankAttnTile)) return hipErrorInvalidValue;
-    if (tile == kRankAttnTile)
+    if (D != kD || (tile != kLongRankAttnTile && tile != kRankAttnTile && tile != kSmallRankAttnTile))
+        return hipErrorInvalidValue;
+    const int4* w = reinterpret_cast<const int4*>(work);
+    const int64_t ld = (int64_t)3 * H * kD;
+    if (tile == kLongRankAttnTile)
+        k_attn_mfma<false, kRankQG, false, 8><<<(unsigned)items, 512, 0, s>>>(
+            qkv, ld, o, nullptr, row0, H, w, cache_k, cache_v, cache_cap, force_exact_flag());
+    else if (tile == kRankAttnTile)
         k_attn_mfma<false, kRankQG><<<(unsigned)items, 256, 0, s>>>(
-            qkv, (int64_t)3 * H * kD, o, nullptr, row0, H,
-            reinterpret_cast<const int4*>(work), cache_k, cache_v, cache_cap, force_exact_flag());
+            qkv, ld, o, nullptr, row0, H, w, cache_k, cache_v, cache_cap, force_exact_flag());
     else
         k_attn_mfma<false, kSmallRankQG><<<(unsigned)items, 256, 0, s>>>(
-            qkv, (int64_t)3 * H * kD, o, nullptr, row0, H,
-            reinterpret_cast<const int4*>(work), cache_k, cache_v, cache_cap, force_exact_flag());
+            qkv, ld, o, nullptr, row0, H, w, cache_k, cache_v, cache_cap, force_exact_flag());
     return hipGetLastError();
 }
 
@@ -580,16 +592,20 @@ hipError_t launch_attn_rank_mx(const bf16* qkv, uint8_t* codes, uint8_t* scales,
                                int64_t items, int tile, const bf16* cache_k, const bf16* cache_v,
                                int64_t cache_cap, hipStream_t s) {
     if (items == 0) return hipSuccess;
-    if (D != kD || (tile != kRankAttnTile && tile != kSmallRankAttnTile) || scales == nullptr)
+    if (D != kD || (tile != kLongRankAttnTile && tile != kRankAttnTile && tile != kSmallRankAttnTile) ||
+        scales == nullptr)
         return hipErrorInvalidValue;
-    if (tile == kRankAttnTile)
+    const int4* w = reinterpret_cast<const int4*>(work);
+    const int64_t ld = (int64_t)3 * H * kD;
+    if (tile == kLongRankAttnTile)
+        k_attn_mfma<false, kRankQG, true, 8><<<(unsigned)items, 512, 0, s>>>(
+            qkv, ld, codes, scales, row0, H, w, cache_k, cache_v, cache_cap, force_exact_flag());
+    else if (tile == kRankAttnTile)
         k_attn_mfma<false, kRankQG, true><<<(unsigned)items, 256, 0, s>>>(
-            qkv, (int64_t)3 * H * kD, codes, scales, row0, H,
-            reinterpret_cast<const int4*>(work), cache_k, cache_v, cache_cap, force_exact_flag());
+            qkv, ld, codes, scales, row0, H, w, cache_k, cache_v, cache_cap, force_exact_flag());
     else
         k_attn_mfma<false, kSmallRankQG, true><<<(unsigned)items, 256, 0, s>>>(
-            qkv, (int64_t)3 * H * kD, codes, scales, row0, H,
-            reinterpret_cast<const int4*>(work), cache_k, cache_v, cache_cap, force_exact_flag());
+            qkv, ld, codes, scales, row0, H, w, cache_k, cache_v, cache_cap, force_exact_flag());
     return hipGetLastError();
 }
 

@@ -911,7 +911,7 @@ size_t upr_rank_workspace_bytes(const upr_model* m, const upr_segments* hist,
     if (check_segments(hist, "hist", &hf, &hl) != UPR_OK) return 0;
     if (check_segments(cand, "cand", &cf, &cl) != UPR_OK) return 0;
     if (hist->num_users != cand->num_users) return 0;
-    return upr::plan_rank(m->cfg, cand->num_users, cand->offsets_host).bytes;
+    return upr::plan_rank(m->cfg, cand->num_users, cand->offsets_host, hist->offsets_host).bytes;
 }
 
 upr_status upr_encode_user(const upr_model* m, const void* hist_emb, const upr_segments* hist,
@@ -966,7 +966,7 @@ static upr_status rank_entry(const upr_model* m, const upr_kv_cache* cache,
         if (!scores) return fail(UPR_ERR_NULL, "scores is NULL");
         if (hl > hf && !cache->data) return fail(UPR_ERR_NULL, "cache data is NULL");
     }
-    const upr::RankPlan p = upr::plan_rank(m->cfg, cand->num_users, cand->offsets_host);
+    const upr::RankPlan p = upr::plan_rank(m->cfg, cand->num_users, cand->offsets_host, hist->offsets_host);
     if (scratch) {
         if (p.bytes > UPR_NOALLOC_SCRATCH_BYTES)
             return fail(UPR_ERR_LIMIT, "the call needs a %zu-byte workspace; the no-alloc scratch "
@@ -1087,7 +1087,8 @@ size_t upr_rank_actions_workspace_bytes(const upr_model* m, const upr_heads* hd,
     if (check_segments(hist, "hist", &hf, &hl) != UPR_OK) return 0;
     if (check_segments(cand, "cand", &cf, &cl) != UPR_OK) return 0;
     if (hist->num_users != cand->num_users) return 0;
-    return upr::plan_rank(m->cfg, cand->num_users, cand->offsets_host, hd->C * hd->Fh).bytes;
+    return upr::plan_rank(m->cfg, cand->num_users, cand->offsets_host, hist->offsets_host,
+                          hd->C * hd->Fh).bytes;
 }
 
 upr_status upr_rank_actions(const upr_model* m, const upr_heads* hd, const upr_kv_cache* cache,
@@ -1116,7 +1117,8 @@ upr_status upr_rank_actions(const upr_model* m, const upr_heads* hd, const upr_k
         if (!cand_emb) return fail(UPR_ERR_NULL, "cand_emb is NULL");
         if (hl > hf && !cache->data) return fail(UPR_ERR_NULL, "cache data is NULL");
     }
-    const upr::RankPlan p = upr::plan_rank(m->cfg, cand->num_users, cand->offsets_host, hd->C * hd->Fh);
+    const upr::RankPlan p = upr::plan_rank(m->cfg, cand->num_users, cand->offsets_host, hist->offsets_host,
+                                           hd->C * hd->Fh);
     st = check_workspace(ws, ws_bytes, p.bytes);
     if (st != UPR_OK) return st;
     if (p.rows == 0) return ok();

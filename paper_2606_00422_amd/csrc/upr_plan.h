@@ -18,6 +18,11 @@ constexpr int kAttnTile = 128;
 constexpr int kRankAttnTile = 128;
 constexpr int kSmallRankAttnTile = 64;      // ranking calls with few work items
 constexpr int64_t kSmallRankItems = 512;    // fewer 128-candidate items than this
+// Ranking calls whose candidates see long histories (on average at least
+// kLongHistory rows each) take 256-candidate items, eight waves per
+// workgroup: each K/V stage then serves twice the queries.
+constexpr int kLongRankAttnTile = 256;
+constexpr double kLongHistory = 4096.0;
 constexpr bool kHaveMfmaAttn = true;
 
 struct EncodePlan {
@@ -84,7 +89,8 @@ inline EncodePlan plan_encode(const upr_config& c, int U, const int32_t* hoffs) 
 // MXFP8 encodings in the LayerNorm-output and FFN-hidden buffers (codes,
 // then scales at the next 256-byte boundary: rows x cols x 2 bytes hold
 // both for rows x cols >= 256).
-inline RankPlan plan_rank(const upr_config& c, int U, const int32_t* coffs, int head_cols = 0) {
+inline RankPlan plan_rank(const upr_config& c, int U, const int32_t* coffs, const int32_t* hoffs,
+                          int head_cols = 0) {
     RankPlan p;
     p.row0 = coffs[0];
     p.rows = (int64_t)coffs[U] - coffs[0];
@@ -92,10 +98,19 @@ inline RankPlan plan_rank(const upr_config& c, int U, const int32_t* coffs, int 
     const size_t es = dtype_bytes(c), R = (size_t)p.rows, d = c.d_model, F = c.d_ff;
     p.use_mfma_attn = use_mfma_attn(c);
     if (p.use_mfma_attn) {
-        p.work_items = attn_items(c, U, coffs, p.attn_tile);
-        if (p.work_items < kSmallRankItems) {
-            p.attn_tile = kSmallRankAttnTile;
+        double seen = 0.0;                  // history rows seen, summed over candidates
+        for (int u = 0; u < U; ++u)
+            seen += (double)((int64_t)coffs[u + 1] - coffs[u]) * (double)((int64_t)hoffs[u + 1] - hoffs[u]);
+        const int64_t long_items = attn_items(c, U, coffs, kLongRankAttnTile);
+        if (seen >= kLongHistory * (double)p.rows && long_items >= kSmallRankItems) {
+            p.attn_tile = kLongRankAttnTile;
+            p.work_items = long_items;
+        } else {
             p.work_items = attn_items(c, U, coffs, p.attn_tile);
+            if (p.work_items < kSmallRankItems) {
+                p.attn_tile = kSmallRankAttnTile;
+                p.work_items = attn_items(c, U, coffs, p.attn_tile);
+            }
         }
     }
     size_t o = 0;

@@ -455,13 +455,15 @@ __global__ __launch_bounds__(1024) void k_rank_worklist(const int32_t* __restric
                                                         int4* __restrict__ work, int64_t items,
                                                         int64_t row_first, int64_t row_last,
                                                         int64_t cap) {
+    constexpr int kWaves = 1024 / 64;
     __shared__ int s_len[kSortMax];
-    __shared__ int s_tiles[kSortMax];     // tiles of the user at each rank
     __shared__ int s_user[kSortMax];      // user at each rank
     __shared__ int s_scan[1024];          // inclusive scan of tiles over the chunk's ranks
-    __shared__ int s_cu[1024];            // user of each rank of the chunk
+    __shared__ int4 s_seg[1024];          // per rank of the chunk: history start and length, candidate start and count
+    __shared__ long long s_wtot[kWaves];
+    __shared__ int s_wsum[kWaves];
     __shared__ long long s_carry;
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     {
         bool bad = false;
         long long tiles = 0;
@@ -471,14 +473,16 @@ __global__ __launch_bounds__(1024) void k_rank_worklist(const int32_t* __restric
             if (c1 >= c0) tiles += (c1 - c0 + tile - 1) / tile;
         }
         if (tid == 0) bad |= coffs[0] != row_first || coffs[U] != row_last;
-        // the tile total, reduced over the workgroup through LDS
-        s_scan[tid] = (int)min(tiles, (long long)(1 << 30));
+        // the tile total: wave sums, then thread 0 adds the waves'
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) tiles += __shfl_xor(tiles, off, 64);
+        if (lane == 0) s_wtot[wv] = tiles;
         __syncthreads();
-        for (int off = 512; off > 0; off >>= 1) {
-            if (tid < off) s_scan[tid] = (int)min((long long)s_scan[tid] + s_scan[tid + off], (long long)(1 << 30));
-            __syncthreads();
+        if (tid == 0) {
+            long long t = 0;
+            for (int w = 0; w < kWaves; ++w) t += s_wtot[w];
+            bad |= t > (1ll << 40) || t * H != items;
         }
-        if (tid == 0) bad |= (long long)s_scan[0] * H != items;
         if (__syncthreads_or(bad)) {
             for (int64_t i = tid; i < items; i += 1024) work[i] = make_int4(0, 0, 0, 0);
             return;
@@ -496,54 +500,56 @@ __global__ __launch_bounds__(1024) void k_rank_worklist(const int32_t* __restric
                 rank += (nv > nu) || (nv == nu && v < u);
             }
             s_user[rank] = u;
-            s_tiles[rank] = (coffs[u + 1] - coffs[u] + tile - 1) / tile;
         }
         __syncthreads();
     }
     if (tid == 0) s_carry = 0;
     __syncthreads();
-    // chunked scan of tiles in rank order; the chunk's items are then written
-    // by all threads, each finding its tile's rank by binary search
+    // Chunks of 1024 ranks: each thread reads its rank's segments once, the
+    // tile counts are scanned (within waves by shuffles, then across the
+    // sixteen wave totals), and each thread writes the H items of its tiles,
+    // finding a tile's rank by binary search on the scan.
     for (int base = 0; base < U; base += 1024) {
         const int r = base + tid;
-        int u = -1, t = 0;
+        int t = 0;
+        int4 seg = make_int4(0, 0, 0, 0);
         if (r < U) {
-            u = sorted ? s_user[r] : r;
-            t = sorted ? s_tiles[r] : (coffs[r + 1] - coffs[r] + tile - 1) / tile;
+            const int u = sorted ? s_user[r] : r;
+            const int c0 = coffs[u], h0 = hoffs[u];
+            seg = make_int4(h0, hoffs[u + 1] - h0, c0, coffs[u + 1] - c0);
+            t = (seg.w + tile - 1) / tile;
         }
-        s_scan[tid] = t;
+        s_seg[tid] = seg;
+        int v = t;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int y = __shfl_up(v, off, 64);
+            if (lane >= off) v += y;
+        }
+        if (lane == 63) s_wsum[wv] = v;
         __syncthreads();
-        for (int off = 1; off < 1024; off <<= 1) {
-            const int v = tid >= off ? s_scan[tid - off] : 0;
-            __syncthreads();
-            s_scan[tid] += v;
-            __syncthreads();
-        }
-        s_cu[tid] = u;
+        for (int w = 0; w < wv; ++w) v += s_wsum[w];
+        s_scan[tid] = v;
         __syncthreads();
         const int total = s_scan[1023];                 // tiles of this chunk
         const int nr = min(1024, U - base);             // ranks of this chunk
-        for (long long it = tid; it < (long long)total * H; it += 1024) {
-            const int x = (int)(it / H), hh = (int)(it % H);
+        for (int x = tid; x < total; x += 1024) {
             int lo = 0, hi = nr - 1;                    // smallest rank with s_scan > x
             while (lo < hi) {
                 const int mid = (lo + hi) >> 1;
                 if (s_scan[mid] > x) hi = mid; else lo = mid + 1;
             }
-            const int ur = s_cu[lo];
+            const int4 sg = s_seg[lo];
             const int tr = s_scan[lo] - (lo > 0 ? s_scan[lo - 1] : 0);
             const int j = x - (s_scan[lo] - tr);
-            const long long idx = (long long)H * (s_carry + x) + hh;
-            if (idx < items) {
-                const int k = coffs[ur + 1] - coffs[ur];
-                const int tt = reverse ? tr - 1 - j : j;
-                const int cnt = min(tile, k - tt * tile);
-                work[idx] = make_int4(hoffs[ur], hoffs[ur + 1] - hoffs[ur], coffs[ur] + tt * tile,
-                                      hh | (cnt << 16));
-            }
+            const int tt = reverse ? tr - 1 - j : j;
+            const int cnt = min(tile, sg.w - tt * tile);
+            const long long idx0 = (long long)H * (s_carry + x);
+            for (int hh = 0; hh < H; ++hh)
+                if (idx0 + hh < items) work[idx0 + hh] = make_int4(sg.x, sg.y, sg.z + tt * tile, hh | (cnt << 16));
         }
         __syncthreads();
-        if (tid == 1023) s_carry += total;
+        if (tid == 0) s_carry += total;
         __syncthreads();
     }
 }

@@ -109,7 +109,9 @@ __device__ __forceinline__ float quad_sum(float v) {
 // are history rows of qsrc = query rows (stride d), own keys in the cache.
 // MXO: the output goes out as MXFP8 (codes in `out`, one E8M0 byte per
 // 32-value block in `out_scales`), encoded from the fp32 values, for the fp8
-// projection variant; else fp16.
+// projection variant; else fp16.  kW: waves per workgroup, four, or eight
+// for ranking over long histories (256-candidate items, two workgroups per
+// CU, so still four waves per SIMD).
 template <bool CAUSAL, int kQG, bool MXO = false, int kW = 4>
 __global__ __launch_bounds__(64 * kW, kW == 8 ? 2 : (8 / kQG < 4 ? 8 / kQG : 4)) void k_attn_mfma(
     const bf16* __restrict__ qsrc, int64_t qstride, void* __restrict__ out,

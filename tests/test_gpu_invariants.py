@@ -86,16 +86,18 @@ def test_tile_height_does_not_change_scores():
         assert np.array_equal(s[co[u]:co[u + 1]], batch[co[u]:co[u + 1]]), f"user {u}"
 
 
-def test_long_history_items_do_not_change_scores():
+@pytest.mark.parametrize("model_dtype", ["bf16", "bf16_mxfp8"])
+def test_long_history_items_do_not_change_scores(model_dtype):
     """Candidates that see 4,096+ history rows on average take 256-candidate
     attention items (eight waves per workgroup); single users of the same
     batch take 64-candidate items.  Every query's softmax and P.V run over
     the same keys in the same order either way, so the scores agree bit for
-    bit, and a sample of them agrees with the oracle."""
+    bit (also in the fp8 variant, whose attention writes MXFP8), and for
+    bf16 a sample of them agrees with the oracle."""
     hl, k = [4608, 4100, 5000, 4700], 4096
     inp = make_inputs(hl, [k] * len(hl), 512, 8, 1, 2048, dtype="bf16", seed=37, variant="perturbed")
-    say(f"[gpu] long-history items: {len(hl)} users x {k} candidates, histories {hl}")
-    run = GpuRun(inp)
+    say(f"[gpu] long-history items ({model_dtype}): {len(hl)} users x {k} candidates, histories {hl}")
+    run = GpuRun(inp, model_dtype=model_dtype)
     run.encode()
     run.rank()
     batch = run.scores_np().copy()
@@ -106,6 +108,8 @@ def test_long_history_items_do_not_change_scores():
         run.rank(hoff=np.array([ho[u], ho[u + 1]], np.int32), coff=np.array([co[u], co[u + 1]], np.int32))
         s = run.scores_np()
         assert np.array_equal(s[co[u]:co[u + 1]], batch[co[u]:co[u + 1]]), f"user {u}"
+    if model_dtype != "bf16":
+        return
     # a sample of user 1's candidates against the oracle
     rows = co[1] + np.arange(0, k, 257)
     cache = oracle.encode(inp.weights, inp.d, inp.H, inp.L, inp.F, inp.hist_emb, inp.hist_offsets,
